@@ -1,0 +1,98 @@
+"""Pure-Python brute force of the PSS layer on tiny inputs.
+
+TEST INFRASTRUCTURE ONLY.  Independent of ``pss_oracle``: Python integers
+for the hash (no key mod p pre-reduction, no NumPy), explicit loops, and the
+linear-sketch form of Thm. 2 / Sec. 2.4:
+
+    virtual table row of (t, i):  V[(t, i)] = (S e_(t,i))^T w
+    forward:   out[b, t*d + c] = sum over items i of bag (t, b) of V[(t, i)][c]
+    backward:  G = S^T (dL/dV)                       (Alg. 1, dense branch)
+
+S has one row per (table, token, output dim) and one column per element of
+the flat array; its entry is 1 where the ROBE-Z mapping (Sec. 2.5) reads that
+element, so every row holds exactly one 1.
+"""
+from __future__ import annotations
+
+P = 2**31 - 1
+
+
+def base(a, b, M, T, C, t, i, j):
+    """h(i, j) = ((a * key + b) mod p) mod M with key = (i*T + t)*C + j."""
+    key = (i * T + t) * C + j
+    return ((a * key + b) % P) % M
+
+
+def sketch_rows(M, Z, d, T, rows_per_table, a, b):
+    """Explicit S as a dict {(t, i, c): column of the single 1}.
+
+    Column = (h(i, c // Z) + c % Z) mod M.  Also returned as a dense list of
+    lists (rows ordered by (t, i, c)) to make S e_i a literal matrix product.
+    """
+    C = d // Z
+    col = {}
+    for t in range(T):
+        for i in range(rows_per_table[t]):
+            for c in range(d):
+                col[(t, i, c)] = (base(a, b, M, T, C, t, i, c // Z) + c % Z) % M
+    return col
+
+
+def dense_S(M, Z, d, T, rows_per_table, a, b):
+    """S as a list of 0/1 rows, row index r(t, i, c) in lexicographic order."""
+    col = sketch_rows(M, Z, d, T, rows_per_table, a, b)
+    keys = sorted(col)
+    S = []
+    for k in keys:
+        row = [0] * M
+        row[col[k]] = 1
+        S.append(row)
+    return keys, S
+
+
+def virtual_table(w, M, Z, d, T, rows_per_table, a, b):
+    """V[(t, i)] = (S e_(t,i))^T w as lists of floats, via the dense S."""
+    keys, S = dense_S(M, Z, d, T, rows_per_table, a, b)
+    V = {}
+    for r, (t, i, c) in enumerate(keys):
+        V.setdefault((t, i), [0.0] * d)
+        V[(t, i)][c] = sum(S[r][m] * float(w[m]) for m in range(M))
+    return V
+
+
+def forward(w, M, Z, d, T, B, rows_per_table, a, b, indices, offsets):
+    """Pooled embeddings [B][T*d] as Python floats (exact sums of doubles)."""
+    V = virtual_table(w, M, Z, d, T, rows_per_table, a, b)
+    out = [[0.0] * (T * d) for _ in range(B)]
+    for t in range(T):
+        for bb in range(B):
+            g = t * B + bb
+            for e in range(int(offsets[g]), int(offsets[g + 1])):
+                i = int(indices[e])
+                for c in range(d):
+                    out[bb][t * d + c] += V[(t, i)][c]
+    return out
+
+
+def gradient(M, Z, d, T, B, rows_per_table, a, b, indices, offsets, grad_out):
+    """G = S^T (dL/dV) with dL/dV[(t, i)][c] = sum of grad_out over the bags
+    that contain token i of table t (with multiplicity).  Returns (G, cnt)."""
+    keys, S = dense_S(M, Z, d, T, rows_per_table, a, b)
+    dV = {k: 0.0 for k in keys}
+    reads = {k: 0 for k in keys}
+    for t in range(T):
+        for bb in range(B):
+            g = t * B + bb
+            for e in range(int(offsets[g]), int(offsets[g + 1])):
+                i = int(indices[e])
+                for c in range(d):
+                    dV[(t, i, c)] += float(grad_out[bb][t * d + c])
+                    reads[(t, i, c)] += 1
+    G = [0.0] * M
+    cnt = [0] * M
+    for r, k in enumerate(keys):
+        for m in range(M):
+            if S[r][m]:
+                G[m] += dV[k]
+                cnt[m] += reads[k]
+    return G, cnt

@@ -1,0 +1,224 @@
+"""Benchmark of the PSS hashed-embedding layer on one MI355X.
+
+One step = pss_forward + pss_backward_update (forward gather/pool, backward
+deposit, optimizer step) over one batch of synthetic bags, rotating 4
+pre-generated index batches and gradient batches resident in HBM.
+
+Default workload: criteo-tb-shaped one-hot batch (26 tables with log-uniform
+cardinalities in [3, 4e7], Zipf(1.1) indices, batch 65536, d = 128, Z = 32,
+shared float32 array of 2.5e6 weights = 10 MB, SGD).
+
+Prints one JSON line on stdout; diagnostics go to stderr.
+  value          lookups/s over the timed steps (lookup = one (sample, table,
+                 index) row: d gathered, pooled, d deposited)
+  roofline       the dominant kernel's algorithmic HBM bytes per launch over
+                 its average duration (HIP events on the launch stream) vs the
+                 8 TB/s HBM peak; step_* fields give the same for the whole step
+  cpu_baseline   the CPU oracle timed on a prefix of the same batch
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+ROTATE = 4
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def hbm_bytes(wl, B, N):
+    """Algorithmic HBM bytes of one forward and one backward launch.
+
+    Forward: indices (8 B each) + offsets (8 B per bag + 1) + pooled output
+    (4 B per element).  Backward: the same index/offset stream + the output
+    gradient (4 B per element).  The gathered and deposited array traffic is
+    counted at the array's own level (L2/MALL when resident), not here.
+    """
+    stream = 8 * N + 8 * (wl.T * B + 1)
+    rows = 4 * B * wl.T * wl.d
+    return stream + rows, stream + rows
+
+
+def optimizer_bytes(wl):
+    """Dense optimizer pass over M when one runs (Adagrad or bf16 storage):
+    zero-fill G (4 B write) + read G (4) + read/write w + read/write s."""
+    if wl.optimizer == "sgd" and wl.weight_dtype == "f32":
+        return 0
+    wsz = 2 if wl.weight_dtype == "bf16" else 4
+    state = 8 if wl.optimizer == "adagrad" else 0
+    return wl.M * (4 + 4 + 2 * wsz + state)
+
+
+def cpu_baseline(wl, x, a, b, budget_s=12.0):
+    """Times the CPU oracle (forward + gradient + update, float64) on the first
+    B' samples of batch 0, B' doubled until one pass takes >= budget/4."""
+    import synth
+    from oracle import pss_oracle as o
+    w = synth.make_weights(wl)
+    s = np.zeros(wl.M, dtype=np.float32) if wl.optimizer == "adagrad" else None
+    Bp = 256
+    best = None
+    spent = 0.0
+    while True:
+        lens = np.diff(x.offsets).reshape(wl.T, x.B)[:, :Bp]
+        off = np.zeros(wl.T * Bp + 1, dtype=np.int64)
+        np.cumsum(lens.ravel(), out=off[1:])
+        starts = x.offsets[:-1].reshape(wl.T, x.B)[:, :Bp]
+        idx = np.concatenate([x.indices[st:st + ln] for st, ln in zip(starts.ravel(), lens.ravel())])
+        g = np.random.default_rng(7).standard_normal((Bp, wl.T * wl.d), dtype=np.float32)
+        t0 = time.perf_counter()
+        o.forward64(w, wl.M, wl.Z, wl.d, wl.T, Bp, a, b, idx, off, wl.weight_dtype)
+        o.backward_update(w, s, wl.M, wl.Z, wl.d, wl.T, Bp, a, b, idx, off, g, wl.lr, wl.eps,
+                          wl.weight_dtype)
+        dt = time.perf_counter() - t0
+        spent += dt
+        best = (idx.shape[0], dt, Bp)
+        if dt >= budget_s / 4 or Bp >= x.B or spent + 2 * dt > budget_s:
+            break
+        Bp *= 2
+    n, dt, Bp = best
+    return {"value": n / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {Bp} of {x.B} samples of batch 0 ({n} lookups, all {wl.T} tables), "
+                      f"one forward+gradient+update pass, float64 NumPy, single thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the layer's multi-GPU "
+              f"sharding is a design note, not a measured path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2207_10731_amd import pss
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    wl = synth.get(args.config)
+    flags = {"auto": pss.PSS_BWD_AUTO, "atomic": pss.PSS_BWD_ATOMIC,
+             "sorted": pss.PSS_BWD_SORTED}[args.variant]
+    dt_code = pss.PSS_BF16 if wl.weight_dtype == "bf16" else pss.PSS_F32
+
+    t0 = time.perf_counter()
+    xs = [synth.make_inputs(wl, batch=k) for k in range(ROTATE)]
+    log(f"[bench] {wl.name}: inputs generated in {time.perf_counter() - t0:.1f}s; "
+        f"N per batch {[x.N for x in xs]}")
+    w = synth.make_weights(wl)
+    if wl.weight_dtype == "bf16":
+        shared = torch.from_numpy(w.view(np.int16)).to(dev).view(torch.bfloat16)
+    else:
+        shared = torch.from_numpy(w).to(dev)
+    state = torch.zeros(wl.M, dtype=torch.float32, device=dev) if wl.optimizer == "adagrad" else None
+    idx = [torch.from_numpy(x.indices).to(dev) for x in xs]
+    off = [torch.from_numpy(x.offsets).to(dev) for x in xs]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.data_seed)
+    grads = [torch.randn((wl.B, wl.T * wl.d), generator=gen, device=dev) for _ in range(ROTATE)]
+    out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=dev)
+    hps = [pss.make_hash_params(wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=x.N,
+                                weight_dtype=dt_code, eps=wl.eps, flags=flags) for x in xs]
+    torch.cuda.synchronize()
+
+    def step(k, ev=None):
+        r = k % ROTATE
+        if ev is not None:
+            ev[0].record()
+        pss.pss_forward(shared, wl.M, wl.Z, wl.d, hps[r], idx[r], off[r], out)
+        if ev is not None:
+            ev[1].record()
+        pss.pss_backward_update(shared, state, wl.M, wl.Z, wl.d, hps[r], idx[r], off[r], grads[r],
+                                wl.lr)
+        if ev is not None:
+            ev[2].record()
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(k, evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    bwd_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    lookups = sum(xs[k % ROTATE].N for k in range(args.steps))
+    value = lookups / wall
+    ms_per_step = 1e3 * wall / args.steps
+    N_avg = lookups / args.steps
+
+    fb, bb = hbm_bytes(wl, wl.B, N_avg)
+    ob = optimizer_bytes(wl)
+    f_avg, b_avg = fwd_ms.mean() * 1e-3, bwd_ms.mean() * 1e-3
+    kern = {"forward": (fb, f_avg), "backward_update": (bb + ob, b_avg)}
+    dom = max(kern, key=lambda k: kern[k][1])
+    dom_bytes, dom_t = kern[dom]
+    achieved = dom_bytes / dom_t / 1e9
+    step_bytes = fb + bb + ob
+    t_star = step_bytes / (HBM_PEAK_GBS * 1e9)
+    log(f"[bench] forward   median {np.median(fwd_ms)*1e3:.1f} us  p10 {np.percentile(fwd_ms,10)*1e3:.1f}"
+        f"  p90 {np.percentile(fwd_ms,90)*1e3:.1f}  -> {fb/f_avg/1e9:.0f} GB/s (HBM algorithmic)")
+    log(f"[bench] backward  median {np.median(bwd_ms)*1e3:.1f} us  p10 {np.percentile(bwd_ms,10)*1e3:.1f}"
+        f"  p90 {np.percentile(bwd_ms,90)*1e3:.1f}  -> {(bb+ob)/b_avg/1e9:.0f} GB/s (HBM algorithmic)")
+    log(f"[bench] step {ms_per_step*1e3:.1f} us, T* {t_star*1e6:.1f} us, frac {t_star/(wall/args.steps):.3f}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import pss_oracle as o
+        a, b = o.hash_params_from_seed(wl.hash_seed)
+        t0 = time.perf_counter()
+        cpu = cpu_baseline(wl, xs[0], a, b)
+        log(f"[bench] cpu baseline {cpu['value']:.3e} lookups/s in {time.perf_counter()-t0:.1f}s")
+
+    rec = {
+        "metric": "hashed-embedding lookups/sec (fwd+bwd+update) + achieved GB/s vs roofline",
+        "value": value,
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if wl.weight_dtype == "f32" else "bf16-storage/f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "tables": wl.T, "batch": wl.B, "d": wl.d, "Z": wl.Z,
+                   "M": wl.M, "storage": wl.weight_dtype, "optimizer": wl.optimizer,
+                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant,
+                   "lookups_per_step": N_avg},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": dom_bytes, "avg_launch_us": dom_t * 1e6,
+                     "step_hbm_bytes": step_bytes, "step_t_star_us": t_star * 1e6,
+                     "step_frac": t_star / (wall / args.steps),
+                     "forward_us": f_avg * 1e6, "backward_update_us": b_avg * 1e6},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

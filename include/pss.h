@@ -1,0 +1,152 @@
+/*
+ * pss.h - C ABI of the hashed shared-memory embedding layer (PSS, ROBE-Z
+ * mapping) for AMD Instinct MI355X (gfx950).
+ *
+ * The layer keeps ONE flat learnable array `shared` of M weights for all T
+ * embedding tables.  Chunk j (dims [jZ, (j+1)Z)) of the embedding of token i
+ * of table t is read from Z consecutive weights starting at a universal-hash
+ * address (paper Sec. 2.5, "HashedNet and ROBE-Z"; universal hashing of the
+ * mapping: Sec. 2.5, "Sparse JL with independence relaxation"):
+ *
+ *     C    = d / Z                          chunks per embedding
+ *     key  = (i * T + t) * C + j            exact 64-bit integer
+ *     h    = ((a * key + b) mod p) mod M    p = 2^31 - 1
+ *     dim jZ + k of the embedding  =  shared[(h + k) mod M],  0 <= k < Z
+ *
+ * Forward (Sec. 2.4, forward(i) = (S e_i)^T M) sum-pools those embeddings
+ * over each bag; backward (Sec. 2.4, backward(i, Delta) = (S e_i) Delta, and
+ * Alg. 1) scatter-adds the output gradient onto the addresses that were read
+ * and applies the optimizer step to `shared` in the same call.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Bags.  There are T*B bags, table-major: bag g = t*B + b holds the token
+ *   indices indices[offsets[g] .. offsets[g+1]) of table t for sample b.
+ *   offsets: int64[T*B + 1], offsets[0] = 0, non-decreasing,
+ *   offsets[T*B] = N.  indices: int64[N], each in [0, 2^31).  Duplicate
+ *   indices in a bag count twice; empty bags pool to zero.
+ * Pooled rows.  out / grad_out are float32 [B][T*d], row-major:
+ *   element (b, t*d + c) belongs to bag t*B + b, embedding dim c.
+ * Shared array.  `shared` holds M elements of the storage type named by
+ *   pss_hash_params.weight_dtype (float32, or bfloat16 bit patterns).
+ *   Arithmetic is float32 throughout; bfloat16 values are widened exactly on
+ *   load and rounded to nearest-even once per update.
+ * Memory.  Every array argument is device memory owned by the caller; the
+ *   library keeps no pointer after the call returns other than in the work it
+ *   enqueued.  Scratch space is taken stream-ordered from a library-owned
+ *   memory pool on the current device and returned on the same stream.
+ * Streams.  Work is enqueued on `stream` (0 = the legacy default stream) of
+ *   the current device; calls return once the work is enqueued.
+ * Errors.  Arguments are checked on the host before anything is enqueued; a
+ *   violation returns PSS_ERR_INVALID_ARG (or PSS_ERR_UNSUPPORTED) and
+ *   enqueues nothing.  A failed launch or runtime call returns PSS_ERR_HIP.
+ *   Contents of device arrays (offsets monotone, indices in range) are
+ *   preconditions that are not checked on the device; whatever they hold,
+ *   every address the kernels touch stays inside the arrays described above
+ *   (hash addresses are reduced mod M; item ranges are clamped to [0, N]).
+ * Threads.  Concurrent calls on different streams are safe.
+ */
+#ifndef PSS_H
+#define PSS_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PSS_PRIME 2147483647u /* p = 2^31 - 1 */
+#define PSS_MAX_DIM 4096      /* largest embedding width d */
+
+typedef enum { PSS_F32 = 0, PSS_BF16 = 1 } pss_dtype;
+
+enum {
+  PSS_OK = 0,
+  PSS_ERR_INVALID_ARG = 1,
+  PSS_ERR_UNSUPPORTED = 2,
+  PSS_ERR_HIP = 3,
+  PSS_ERR_NO_MEMORY = 4
+};
+
+/* Backward variant, bits 0-1 of pss_hash_params.flags.
+ *   AUTO    library's choice for the shape (currently ATOMIC).
+ *   ATOMIC  float atomics into `shared` (SGD, float32 storage) or into a
+ *           float32 gradient scratch followed by one streaming optimizer pass.
+ *           Summation order is not deterministic.
+ *   SORTED  contributions grouped by hashed address and reduced without
+ *           global float atomics (Alg. 1 sparse branch: unique addresses,
+ *           summed values), then the optimizer applied per unique address.
+ *           Bit-identical from run to run. */
+enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2 };
+#define PSS_BWD_MASK 3u
+
+typedef struct {
+  uint32_t a;            /* hash multiplier, 1 <= a <= p - 1 */
+  uint32_t b;            /* hash offset,     0 <= b <= p - 1 */
+  uint32_t num_tables;   /* T >= 1 */
+  uint32_t batch;        /* B >= 1 (bags = T*B, table-major) */
+  int64_t num_indices;   /* N = number of entries of `indices` (= offsets[T*B]) */
+  int32_t weight_dtype;  /* pss_dtype of `shared` */
+  float eps;             /* Adagrad epsilon (ignored by SGD); >= 0 */
+  uint32_t flags;        /* PSS_BWD_* in bits 0-1, other bits must be 0 */
+} pss_hash_params;
+
+/* Fills p->a and p->b from `seed` (other fields untouched): with x1, x2 the
+ * first two outputs of SplitMix64 (Steele, Lea & Flood 2014) started from
+ * state `seed`, a = 1 + (x1 mod (p - 1)) and b = x2 mod p.  Host only.
+ * Returns PSS_ERR_INVALID_ARG if p is NULL. */
+int pss_hash_params_from_seed(uint64_t seed, pss_hash_params* p);
+
+/* Forward: pooled embeddings (paper Sec. 2.4 forward, Sec. 2.5 mapping).
+ *   out[b][t*d + j*Z + k] = sum over e in bag t*B+b of
+ *                           shared[(h(indices[e], t, j) + k) mod M]
+ * shared   device, M elements of hash_params->weight_dtype, read only
+ * M        1 <= M <= p;  Z: 1 <= Z <= M;  d: 1 <= d <= 4096, Z divides d
+ * indices  device int64[N];  offsets: device int64[T*B + 1]
+ * out      device float32[B][T*d], fully overwritten; must not alias inputs
+ * T*(d/Z) must not exceed 2^32. */
+int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
+                const pss_hash_params* hash_params, const int64_t* indices,
+                const int64_t* offsets, float* out, hipStream_t stream);
+
+/* Backward + optimizer step, in place (paper Sec. 2.4 backward, Alg. 1).
+ *   G[m] = sum of grad_out[b][t*d + j*Z + k] over every (item, j, k) whose
+ *          address (h + k) mod M equals m
+ *   state == NULL : SGD       shared[m] -= lr * G[m]
+ *   state != NULL : Adagrad   state[m] += G[m]^2;
+ *                             shared[m] -= lr * G[m] / (sqrt(state[m]) + eps)
+ * Every element that no lookup reads keeps its exact bits.  shared: device, M elements, updated in place.
+ * state: device float32[M] or NULL, updated in place.  grad_out: device
+ * float32[B][T*d], read only.  Other arguments as for pss_forward. */
+int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
+                        const pss_hash_params* hash_params, const int64_t* indices,
+                        const int64_t* offsets, const float* grad_out, float lr,
+                        hipStream_t stream);
+
+/* Writes h(indices[e], t(e), j) for every item e and chunk j:
+ * base_out: device uint32[N][d/Z].  Same arguments and checks as pss_forward;
+ * exists so that hashed addresses can be compared bit for bit. */
+int pss_debug_addresses(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, uint32_t* base_out,
+                        hipStream_t stream);
+
+/* Host evaluation of the same hash code the kernels run (no GPU needed):
+ * base_out[e*C + j] = h(indices[e], t(e), j) for host arrays indices[N],
+ * offsets[T*B+1] and base_out[N*C].  Returns PSS_ERR_INVALID_ARG on bad
+ * arguments or on offsets that are not a valid partition of [0, N). */
+int pss_hash_bases_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, uint32_t* base_out);
+
+/* Host check of a host copy of offsets: offsets[0] == 0, non-decreasing,
+ * offsets[T*B] == N.  Returns PSS_OK or PSS_ERR_INVALID_ARG. */
+int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N);
+
+/* Static, NUL-terminated description of a status code. */
+const char* pss_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PSS_H */

@@ -204,10 +204,9 @@ def forward64(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32):
     out[b, t*d + c] = sum over items e of bag (t, b) of w[addr(e, c)].
     An empty bag gives 0.
     """
-    w64 = widen(w, weight_dtype)
     offsets = np.asarray(offsets, dtype=np.int64)
     addr = element_addresses(M, Z, d, T, B, a, b, indices, offsets)
-    rows = w64[addr]  # [N, d]
+    rows = widen(np.asarray(w)[addr], weight_dtype)  # [N, d]
     out = np.zeros((T * B, d))
     s_abs = np.zeros((T * B, d))
     lengths = np.diff(offsets)
@@ -227,7 +226,7 @@ def forward_at(w, M, Z, d, T, B, a, b, indices, offsets, bags, weight_dtype=F32)
 
     Same sums as ``forward64``; used to check sampled bags of large batches.
     """
-    w64 = widen(w, weight_dtype)
+    w = np.asarray(w)
     offsets = np.asarray(offsets, dtype=np.int64)
     indices = np.asarray(indices, dtype=np.int64)
     bags = np.asarray(bags, dtype=np.int64)
@@ -239,7 +238,7 @@ def forward_at(w, M, Z, d, T, B, a, b, indices, offsets, bags, weight_dtype=F32)
             continue
         t = np.full(hi - lo, g // B, dtype=np.int64)
         addr = addresses_from_bases(M, Z, bases_for(M, Z, d, T, a, b, indices[lo:hi], t))
-        rows = w64[addr]
+        rows = widen(w[addr], weight_dtype)
         out[r] = rows.sum(axis=0)
         s_abs[r] = np.abs(rows).sum(axis=0)
     return out, s_abs

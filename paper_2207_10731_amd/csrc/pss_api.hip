@@ -1,0 +1,221 @@
+// C ABI of the PSS layer: argument checks, parameter set-up, dispatch and the
+// library-owned scratch pool.  Every check runs on the host before anything
+// is enqueued.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+
+#include "../../include/pss.h"
+#include "pss_launch.hpp"
+
+namespace {
+
+using pss::KParams;
+
+constexpr uint64_t kMaxBags = 1ull << 38;
+
+int check_common(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) {
+  if (hp == nullptr) return PSS_ERR_INVALID_ARG;
+  if (M < 1 || M > static_cast<int64_t>(PSS_PRIME)) return PSS_ERR_INVALID_ARG;
+  if (Z < 1 || static_cast<int64_t>(Z) > M) return PSS_ERR_INVALID_ARG;
+  if (d < 1 || d > PSS_MAX_DIM || d % Z != 0) return PSS_ERR_INVALID_ARG;
+  if (hp->a < 1 || hp->a > PSS_PRIME - 1) return PSS_ERR_INVALID_ARG;
+  if (hp->b > PSS_PRIME - 1) return PSS_ERR_INVALID_ARG;
+  if (hp->num_tables < 1 || hp->batch < 1) return PSS_ERR_INVALID_ARG;
+  const uint64_t bags = static_cast<uint64_t>(hp->num_tables) * hp->batch;
+  if (bags > kMaxBags) return PSS_ERR_INVALID_ARG;
+  const uint64_t TC = static_cast<uint64_t>(hp->num_tables) * static_cast<uint64_t>(d / Z);
+  if (TC >= (1ull << 32)) return PSS_ERR_INVALID_ARG;
+  if (hp->num_indices < 0) return PSS_ERR_INVALID_ARG;
+  if (hp->weight_dtype != PSS_F32 && hp->weight_dtype != PSS_BF16) return PSS_ERR_UNSUPPORTED;
+  if (hp->flags & ~PSS_BWD_MASK) return PSS_ERR_INVALID_ARG;
+  return PSS_OK;
+}
+
+KParams make_params(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) {
+  KParams p;
+  const pss::FastMod fm = pss::make_fastmod(static_cast<uint32_t>(M));
+  p.fm_c = fm.c;
+  p.num_bags = static_cast<uint64_t>(hp->num_tables) * hp->batch;
+  p.N = hp->num_indices;
+  p.M = static_cast<uint32_t>(M);
+  p.a = hp->a;
+  p.b = hp->b;
+  p.T = hp->num_tables;
+  p.B = hp->batch;
+  p.C = static_cast<uint32_t>(d / Z);
+  p.Z = static_cast<uint32_t>(Z);
+  p.d = static_cast<uint32_t>(d);
+  p.TC = p.T * p.C;
+  p.row_stride = p.T * p.d;
+  return p;
+}
+
+// One memory pool per device, created on first use, that keeps what it has
+// reserved (release threshold = max) so steady-state calls do not go back to
+// the driver for scratch space.
+std::mutex g_pool_mu;
+std::map<int, hipMemPool_t> g_pools;
+
+hipError_t pool_for_current_device(hipMemPool_t* out) {
+  int dev = 0;
+  hipError_t st = hipGetDevice(&dev);
+  if (st != hipSuccess) return st;
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  auto it = g_pools.find(dev);
+  if (it != g_pools.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  hipMemPoolProps props;
+  memset(&props, 0, sizeof(props));
+  props.allocType = hipMemAllocationTypePinned;
+  props.handleTypes = hipMemHandleTypeNone;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = dev;
+  hipMemPool_t pool = nullptr;
+  st = hipMemPoolCreate(&pool, &props);
+  if (st != hipSuccess) return st;
+  uint64_t threshold = UINT64_MAX;
+  st = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+  if (st != hipSuccess) return st;
+  g_pools[dev] = pool;
+  *out = pool;
+  return hipSuccess;
+}
+
+int scratch_alloc(void** ptr, size_t bytes, hipStream_t stream) {
+  hipMemPool_t pool = nullptr;
+  if (pool_for_current_device(&pool) != hipSuccess) return PSS_ERR_HIP;
+  const hipError_t st = hipMallocFromPoolAsync(ptr, bytes, pool, stream);
+  if (st == hipErrorOutOfMemory) return PSS_ERR_NO_MEMORY;
+  return st == hipSuccess ? PSS_OK : PSS_ERR_HIP;
+}
+
+int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; }
+
+uint64_t splitmix64_next(uint64_t* state) {
+  uint64_t z = (*state += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+}  // namespace
+
+extern "C" {
+
+int pss_hash_params_from_seed(uint64_t seed, pss_hash_params* p) {
+  if (p == nullptr) return PSS_ERR_INVALID_ARG;
+  uint64_t state = seed;
+  const uint64_t x1 = splitmix64_next(&state);
+  const uint64_t x2 = splitmix64_next(&state);
+  p->a = static_cast<uint32_t>(1 + x1 % (PSS_PRIME - 1));
+  p->b = static_cast<uint32_t>(x2 % PSS_PRIME);
+  return PSS_OK;
+}
+
+int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
+                const pss_hash_params* hash_params, const int64_t* indices,
+                const int64_t* offsets, float* out, hipStream_t stream) {
+  const int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  if (shared == nullptr || offsets == nullptr || out == nullptr) return PSS_ERR_INVALID_ARG;
+  if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  return hip_status(pss::launch_forward(shared, hash_params->weight_dtype == PSS_BF16, p, indices,
+                                        offsets, out, stream));
+}
+
+int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
+                        const pss_hash_params* hash_params, const int64_t* indices,
+                        const int64_t* offsets, const float* grad_out, float lr,
+                        hipStream_t stream) {
+  int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  if (shared == nullptr || offsets == nullptr || grad_out == nullptr) return PSS_ERR_INVALID_ARG;
+  if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
+  if (!isfinite(lr)) return PSS_ERR_INVALID_ARG;
+  if (state != nullptr && !(hash_params->eps >= 0.f && isfinite(hash_params->eps)))
+    return PSS_ERR_INVALID_ARG;
+  const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
+  if (variant == PSS_BWD_SORTED) return PSS_ERR_UNSUPPORTED;
+  if (variant == 3) return PSS_ERR_INVALID_ARG;
+
+  const KParams p = make_params(M, Z, d, hash_params);
+  const bool bf16 = hash_params->weight_dtype == PSS_BF16;
+  if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
+
+  if (state == nullptr && !bf16) {
+    // SGD on float32 storage is linear in G: deposit -lr * grad directly.
+    return hip_status(pss::launch_deposit_atomic(static_cast<float*>(shared), -lr, p, indices,
+                                                 offsets, grad_out, stream));
+  }
+  void* G = nullptr;
+  st = scratch_alloc(&G, static_cast<size_t>(M) * sizeof(float), stream);
+  if (st != PSS_OK) return st;
+  float* Gf = static_cast<float*>(G);
+  hipError_t e = pss::launch_zero(Gf, M, stream);
+  if (e == hipSuccess) e = pss::launch_deposit_atomic(Gf, 1.f, p, indices, offsets, grad_out, stream);
+  if (e == hipSuccess)
+    e = pss::launch_optimizer(shared, bf16, state, Gf, M, lr, hash_params->eps, stream);
+  const hipError_t ef = hipFreeAsync(G, stream);
+  if (e != hipSuccess || ef != hipSuccess) return PSS_ERR_HIP;
+  return PSS_OK;
+}
+
+int pss_debug_addresses(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, uint32_t* base_out,
+                        hipStream_t stream) {
+  const int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  if (offsets == nullptr) return PSS_ERR_INVALID_ARG;
+  if (hash_params->num_indices > 0 && (indices == nullptr || base_out == nullptr))
+    return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  return hip_status(pss::launch_debug_addresses(p, indices, offsets, base_out, stream));
+}
+
+int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N) {
+  if (offsets == nullptr || num_bags < 0 || N < 0) return PSS_ERR_INVALID_ARG;
+  if (offsets[0] != 0 || offsets[num_bags] != N) return PSS_ERR_INVALID_ARG;
+  for (int64_t g = 0; g < num_bags; ++g)
+    if (offsets[g + 1] < offsets[g]) return PSS_ERR_INVALID_ARG;
+  return PSS_OK;
+}
+
+int pss_hash_bases_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, uint32_t* base_out) {
+  const int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  const int64_t bags = static_cast<int64_t>(hash_params->num_tables) * hash_params->batch;
+  const int64_t N = hash_params->num_indices;
+  if (pss_validate_offsets_host(offsets, bags, N) != PSS_OK) return PSS_ERR_INVALID_ARG;
+  if (N > 0 && (indices == nullptr || base_out == nullptr)) return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  for (int64_t g = 0; g < bags; ++g) {
+    const uint32_t t = static_cast<uint32_t>(g / p.B);
+    for (int64_t e = offsets[g]; e < offsets[g + 1]; ++e) {
+      const uint32_t i = static_cast<uint32_t>(indices[e]);
+      for (uint32_t j = 0; j < p.C; ++j)
+        base_out[e * p.C + j] = pss::chunk_base(i, t, j, p.C, p.TC, p.a, p.b, p.fm_c, p.M);
+    }
+  }
+  return PSS_OK;
+}
+
+const char* pss_status_string(int status) {
+  switch (status) {
+    case PSS_OK: return "ok";
+    case PSS_ERR_INVALID_ARG: return "invalid argument";
+    case PSS_ERR_UNSUPPORTED: return "unsupported argument combination";
+    case PSS_ERR_HIP: return "HIP runtime or launch failure";
+    case PSS_ERR_NO_MEMORY: return "out of device memory for scratch space";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

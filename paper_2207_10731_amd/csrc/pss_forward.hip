@@ -1,0 +1,133 @@
+// Forward of the PSS layer: hash -> chunk gather -> sum-pool (paper Sec. 2.4
+// forward(i) = (S e_i)^T M with the ROBE-Z mapping of Sec. 2.5).
+//
+// One wavefront per tile of 64 bags.  For each item the hash's item part is
+// evaluated once for the whole wave (scalar unit: the token index is read
+// from a lane with readlane), each lane adds its chunk's constant, reduces
+// mod M and reads its dims.  U items are gathered before any is consumed so
+// that U * EPL loads per lane are in flight.  Pooling runs in registers in
+// item order; a finished bag's row is written with non-temporal stores (the
+// 4 bytes/dim output stream must not evict the shared array from L2/MALL).
+#include "pss_launch.hpp"
+
+namespace pss {
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = readlane_u32(static_cast<uint32_t>(v), lane);
+  const uint32_t hi = readlane_u32(static_cast<uint32_t>(v >> 32), lane);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+template <typename WT, int EPL, int U>
+__global__ __launch_bounds__(kBlockThreads) void forward_kernel(
+    const WT* __restrict__ w, const KParams p, const int64_t* __restrict__ indices,
+    const int64_t* __restrict__ offsets, float* __restrict__ out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+  const uint64_t g0 = wave * kTileBags;
+  if (g0 >= p.num_bags) return;
+  const uint32_t c0 = blockIdx.y * (kWave * EPL);
+
+  uint32_t step[EPL], kk[EPL];
+  bool act[EPL];
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) {
+    const uint32_t c = c0 + lane + kWave * r;
+    act[r] = c < p.d;
+    const uint32_t cc = act[r] ? c : 0;
+    const uint32_t j = cc / p.Z;
+    kk[r] = cc - j * p.Z;
+    step[r] = chunk_step(p.a, j);
+  }
+
+  const Tile tl = load_tile(p, offsets, g0, lane);
+
+  float acc[EPL];
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
+  int cur = -1;  // local bag being pooled (wave-uniform)
+
+  auto store_row = [&](int bag, bool zero) {
+    const uint64_t ro = readlane_u64(tl.row_off, bag) + c0 + lane;
+#pragma unroll
+    for (int r = 0; r < EPL; ++r)
+      if (act[r]) __builtin_nontemporal_store(zero ? 0.f : acc[r], out + ro + kWave * r);
+  };
+
+  for (int64_t blk = tl.E0; blk < tl.E1; blk += kWave) {
+    const int64_t rem = tl.E1 - blk;
+    const int n = rem < kWave ? static_cast<int>(rem) : kWave;
+    const int64_t e = blk + lane;
+    uint32_t idx = 0;
+    if (lane < n) idx = static_cast<uint32_t>(__builtin_nontemporal_load(indices + e));
+    const int bag = bag_of_item(tl, e);
+    const uint32_t tC = __shfl(tl.tC, bag);
+
+    for (int q = 0; q < n; q += U) {
+      float v[U][EPL];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (q + u < n) {
+          const uint32_t i = readlane_u32(idx, q + u);
+          const uint32_t h0 = item_hash(i, readlane_u32(tC, q + u), p.TC, p.a, p.b);
+#pragma unroll
+          for (int r = 0; r < EPL; ++r) {
+            v[u][r] = 0.f;
+            if (act[r]) {
+              const uint32_t base = fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M);
+              v[u][r] = load_weight(w, wrap_add(base, kk[r], p.M));
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (q + u < n) {
+          const int bg = static_cast<int>(readlane_u32(static_cast<uint32_t>(bag), q + u));
+          if (bg != cur) {
+            if (cur >= 0) store_row(cur, false);
+            for (int z = cur + 1; z < bg; ++z) store_row(z, true);
+            cur = bg;
+#pragma unroll
+            for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
+          }
+#pragma unroll
+          for (int r = 0; r < EPL; ++r) acc[r] += v[u][r];
+        }
+      }
+    }
+  }
+  if (cur >= 0) store_row(cur, false);
+  for (int z = cur + 1; z < tl.nb; ++z) store_row(z, true);
+}
+
+template <typename WT, int EPL, int U>
+static hipError_t launch_fwd_t(const WT* w, const KParams& p, const int64_t* indices,
+                               const int64_t* offsets, float* out, hipStream_t stream) {
+  const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
+  const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
+  if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
+  dim3 grid(static_cast<uint32_t>(blocks), slabs);
+  hipLaunchKernelGGL((forward_kernel<WT, EPL, U>), grid, dim3(kBlockThreads), 0, stream, w, p,
+                     indices, offsets, out);
+  return hipGetLastError();
+}
+
+template <typename WT>
+static hipError_t launch_fwd_w(const WT* w, const KParams& p, const int64_t* indices,
+                               const int64_t* offsets, float* out, hipStream_t stream) {
+  if (p.d <= 64) return launch_fwd_t<WT, 1, 16>(w, p, indices, offsets, out, stream);
+  if (p.d <= 128) return launch_fwd_t<WT, 2, 8>(w, p, indices, offsets, out, stream);
+  if (p.d <= 256) return launch_fwd_t<WT, 4, 4>(w, p, indices, offsets, out, stream);
+  return launch_fwd_t<WT, 8, 2>(w, p, indices, offsets, out, stream);
+}
+
+hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const int64_t* indices,
+                          const int64_t* offsets, float* out, hipStream_t stream) {
+  if (bf16)
+    return launch_fwd_w(static_cast<const uint16_t*>(w), p, indices, offsets, out, stream);
+  return launch_fwd_w(static_cast<const float*>(w), p, indices, offsets, out, stream);
+}
+
+}  // namespace pss

@@ -1,0 +1,125 @@
+// Shared pieces of the PSS kernels: launch parameters, the per-wavefront bag
+// tile, storage-type loads/stores.
+//
+// Work decomposition (forward and backward alike).  Bags are cut into tiles
+// of kTileBags consecutive bags (g = t*B + b, table-major); one wavefront owns
+// a tile.  Lane l holds the start offset of bag l of the tile; the tile's
+// items form one contiguous range of `indices`, which the wave walks in
+// blocks of 64 (one index per lane, one coalesced load).  For every item the
+// wave evaluates the hash (the item part is wave-uniform, the chunk part is a
+// per-lane constant) and touches the d embedding elements of the item with
+// lanes spread over the dims: lane l owns dims c = c0 + l + 64 r.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pss_hash.hpp"
+
+namespace pss {
+
+constexpr int kWave = 64;
+constexpr int kTileBags = 64;     // bags per wavefront tile
+constexpr int kBlockThreads = 256;  // 4 wavefronts per workgroup
+constexpr int kWavesPerBlock = kBlockThreads / kWave;
+
+struct KParams {
+  uint64_t fm_c;      // fast-mod constant of M
+  uint64_t num_bags;  // T*B
+  int64_t N;          // number of items
+  uint32_t M;
+  uint32_t a, b;
+  uint32_t T, B;
+  uint32_t C, Z, d;
+  uint32_t TC;        // T*C (< 2^32)
+  uint32_t row_stride;  // T*d: floats per pooled row
+};
+
+// bfloat16 bits <-> float
+__device__ __forceinline__ float bf16_to_f32(uint16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v) << 16);
+}
+
+// Round to nearest, ties to even; NaN stays a (quiet) NaN.
+PSS_HD uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u;
+  __builtin_memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+template <typename WT>
+__device__ __forceinline__ float load_weight(const WT* w, uint32_t m);
+
+template <>
+__device__ __forceinline__ float load_weight<float>(const float* w, uint32_t m) {
+  return w[m];
+}
+
+template <>
+__device__ __forceinline__ float load_weight<uint16_t>(const uint16_t* w, uint32_t m) {
+  return bf16_to_f32(w[m]);
+}
+
+__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), lane));
+}
+
+// Per-wavefront view of one tile of bags.
+struct Tile {
+  uint64_t g0;        // first bag
+  int nb;             // bags in the tile (1..kTileBags)
+  int64_t E0, E1;     // item range [E0, E1) of the tile (clamped to [0, N])
+  int64_t start;      // lane l: first item of bag g0 + l (clamped, monotone)
+  uint32_t tC;        // lane l: t * C of bag g0 + l
+  uint64_t row_off;   // lane l: b * T*d + t*d of bag g0 + l
+};
+
+// Loads the tile's offsets (one coalesced load) and per-bag constants.
+// Offsets are clamped to [0, N] and made monotone within the tile, so item
+// ranges never leave `indices` whatever the offsets array holds.
+__device__ __forceinline__ Tile load_tile(const KParams& p, const int64_t* __restrict__ offsets,
+                                          uint64_t g0, int lane) {
+  Tile tl;
+  tl.g0 = g0;
+  const uint64_t left = p.num_bags - g0;
+  tl.nb = left < static_cast<uint64_t>(kTileBags) ? static_cast<int>(left) : kTileBags;
+  int64_t s = 0;
+  if (lane < tl.nb) s = __builtin_nontemporal_load(offsets + g0 + lane);
+  int64_t e_last = __builtin_nontemporal_load(offsets + g0 + tl.nb);
+  s = s < 0 ? 0 : (s > p.N ? p.N : s);
+  e_last = e_last < 0 ? 0 : (e_last > p.N ? p.N : e_last);
+  // running max over lanes keeps starts monotone (inclusive scan of max)
+  for (int sh = 1; sh < kWave; sh <<= 1) {
+    const int64_t o = __shfl_up(s, sh);
+    if (lane >= sh && o > s) s = o;
+  }
+  if (lane >= tl.nb) s = INT64_MAX;  // sentinel: no bag
+  tl.start = s;
+  const int64_t first = __shfl(s, 0);
+  // largest start among real bags = start of bag nb-1
+  const int64_t last_start = __shfl(s, tl.nb - 1);
+  tl.E0 = first;
+  tl.E1 = e_last < last_start ? last_start : e_last;
+  const uint64_t g = g0 + static_cast<uint64_t>(lane < tl.nb ? lane : 0);
+  const uint32_t t = static_cast<uint32_t>(g / p.B);
+  const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
+  tl.tC = t * p.C;
+  tl.row_off = static_cast<uint64_t>(b) * p.row_stride + static_cast<uint64_t>(t) * p.d;
+  return tl;
+}
+
+// Local bag (0..nb-1) of item e of the tile: the largest l with start[l] <= e.
+// Binary search over the starts held in the lanes (6 cross-lane reads).
+__device__ __forceinline__ int bag_of_item(const Tile& tl, int64_t e) {
+  int lo = 0;
+  for (int step = kWave / 2; step >= 1; step >>= 1) {
+    const int probe = lo + step;
+    const int64_t sp = __shfl(tl.start, probe < kWave ? probe : kWave - 1);
+    if (probe < tl.nb && sp <= e) lo = probe;
+  }
+  return lo;
+}
+
+}  // namespace pss

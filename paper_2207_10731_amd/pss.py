@@ -1,0 +1,192 @@
+"""Python binding of libpss.so (ctypes): argument marshalling only.
+
+The function names are those of the C ABI.  Tensors must be contiguous and
+live on the current GPU; work is enqueued on torch's current stream unless a
+stream is given.  Every computation happens in the HIP library: if it cannot
+be loaded, the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpss.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "pss.h")
+
+PSS_PRIME = 2**31 - 1
+PSS_F32, PSS_BF16 = 0, 1
+PSS_OK, PSS_ERR_INVALID_ARG, PSS_ERR_UNSUPPORTED, PSS_ERR_HIP, PSS_ERR_NO_MEMORY = 0, 1, 2, 3, 4
+PSS_BWD_AUTO, PSS_BWD_ATOMIC, PSS_BWD_SORTED = 0, 1, 2
+
+
+class PssError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+class pss_hash_params(ctypes.Structure):
+    _fields_ = [
+        ("a", ctypes.c_uint32),
+        ("b", ctypes.c_uint32),
+        ("num_tables", ctypes.c_uint32),
+        ("batch", ctypes.c_uint32),
+        ("num_indices", ctypes.c_int64),
+        ("weight_dtype", ctypes.c_int32),
+        ("eps", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libpss.so once.  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with python -m paper_2207_10731_amd.build")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+    hp = ctypes.POINTER(pss_hash_params)
+    lib.pss_hash_params_from_seed.argtypes = [u64, hp]
+    lib.pss_forward.argtypes = [vp, i64, i32, i32, hp, vp, vp, vp, vp]
+    lib.pss_backward_update.argtypes = [vp, vp, i64, i32, i32, hp, vp, vp, vp, ctypes.c_float, vp]
+    lib.pss_debug_addresses.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
+    lib.pss_hash_bases_host.argtypes = [i64, i32, i32, hp, vp, vp, vp]
+    lib.pss_validate_offsets_host.argtypes = [vp, i64, i64]
+    lib.pss_status_string.argtypes = [ctypes.c_int]
+    lib.pss_status_string.restype = ctypes.c_char_p
+    for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
+                 "pss_debug_addresses", "pss_hash_bases_host", "pss_validate_offsets_host"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def header_functions(path: str = HEADER) -> list[str]:
+    """Names of the functions declared in include/pss.h."""
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)  # drop comments
+    return sorted(set(re.findall(r"\b(pss_\w+)\s*\(", text)))
+
+
+def status_string(status: int) -> str:
+    return load_library().pss_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != PSS_OK:
+        raise PssError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _need(t, dtype, name, device=True):
+    if t is None:
+        return
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if device and not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+
+
+def make_hash_params(seed=None, *, a=None, b=None, num_tables, batch, num_indices,
+                     weight_dtype=PSS_F32, eps=1e-10, flags=PSS_BWD_AUTO) -> pss_hash_params:
+    """Fills the parameter block; (a, b) from ``seed`` via pss_hash_params_from_seed."""
+    hp = pss_hash_params(0, 0, num_tables, batch, num_indices, weight_dtype, eps, flags)
+    if seed is not None:
+        _check(load_library().pss_hash_params_from_seed(ctypes.c_uint64(seed), ctypes.byref(hp)),
+               "pss_hash_params_from_seed")
+    if a is not None:
+        hp.a = a
+    if b is not None:
+        hp.b = b
+    return hp
+
+
+def _weight_dtype(shared):
+    return PSS_BF16 if shared.dtype == torch.bfloat16 else PSS_F32
+
+
+def pss_forward(shared, M, Z, d, hash_params, indices, offsets, out, stream=None):
+    lib = load_library()
+    _need(shared, shared.dtype, "shared")
+    if shared.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("shared must be float32 or bfloat16")
+    if hash_params.weight_dtype != _weight_dtype(shared):
+        raise TypeError("hash_params.weight_dtype does not match shared")
+    _need(indices, torch.int64, "indices")
+    _need(offsets, torch.int64, "offsets")
+    _need(out, torch.float32, "out")
+    _check(lib.pss_forward(_ptr(shared), M, Z, d, ctypes.byref(hash_params), _ptr(indices),
+                           _ptr(offsets), _ptr(out), _stream(stream)), "pss_forward")
+    return out
+
+
+def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr,
+                        stream=None):
+    lib = load_library()
+    _need(shared, shared.dtype, "shared")
+    if hash_params.weight_dtype != _weight_dtype(shared):
+        raise TypeError("hash_params.weight_dtype does not match shared")
+    _need(state, torch.float32, "state")
+    _need(indices, torch.int64, "indices")
+    _need(offsets, torch.int64, "offsets")
+    _need(grad_out, torch.float32, "grad_out")
+    _check(lib.pss_backward_update(_ptr(shared), _ptr(state), M, Z, d, ctypes.byref(hash_params),
+                                   _ptr(indices), _ptr(offsets), _ptr(grad_out),
+                                   ctypes.c_float(lr), _stream(stream)), "pss_backward_update")
+
+
+def pss_debug_addresses(M, Z, d, hash_params, indices, offsets, base_out, stream=None):
+    lib = load_library()
+    _need(indices, torch.int64, "indices")
+    _need(offsets, torch.int64, "offsets")
+    _need(base_out, torch.int32, "base_out")  # uint32 bit patterns
+    _check(lib.pss_debug_addresses(M, Z, d, ctypes.byref(hash_params), _ptr(indices),
+                                   _ptr(offsets), _ptr(base_out), _stream(stream)),
+           "pss_debug_addresses")
+    return base_out
+
+
+def pss_hash_bases_host(M, Z, d, hash_params, indices, offsets):
+    """Host evaluation of the library's hash code on NumPy arrays: uint32 [N, C]."""
+    import numpy as np
+    lib = load_library()
+    idx = np.ascontiguousarray(indices, dtype=np.int64)
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    out = np.zeros((idx.shape[0], d // Z if Z > 0 and d % Z == 0 else 1), dtype=np.uint32)
+    _check(lib.pss_hash_bases_host(M, Z, d, ctypes.byref(hash_params),
+                                   idx.ctypes.data_as(ctypes.c_void_p),
+                                   off.ctypes.data_as(ctypes.c_void_p),
+                                   out.ctypes.data_as(ctypes.c_void_p)), "pss_hash_bases_host")
+    return out
+
+
+def pss_validate_offsets_host(offsets, num_bags, N) -> int:
+    import numpy as np
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    return load_library().pss_validate_offsets_host(off.ctypes.data_as(ctypes.c_void_p),
+                                                    num_bags, N)
+
+
+def pss_status_string(status: int) -> str:
+    return status_string(status)

@@ -70,14 +70,16 @@ enum {
 };
 
 /* Backward variant, bits 0-1 of pss_hash_params.flags.
- *   AUTO    library's choice for the shape (currently ATOMIC).
- *   ATOMIC  float atomics into `shared` (SGD, float32 storage) or into a
- *           float32 gradient scratch followed by one streaming optimizer pass.
- *           Summation order is not deterministic.
- *   SORTED  contributions grouped by hashed address and reduced without
- *           global float atomics (Alg. 1 sparse branch: unique addresses,
- *           summed values), then the optimizer applied per unique address.
- *           Bit-identical from run to run. */
+ *   AUTO    library's choice for the shape (currently SORTED).
+ *   ATOMIC  every (lookup, dim) contribution added with a float atomic, into
+ *           `shared` (SGD on float32 storage) or into a float32 gradient
+ *           buffer followed by one streaming optimizer pass.
+ *   SORTED  Alg. 1 sparse branch: lookups are grouped by token (radix sort on
+ *           the item hash), the output-gradient rows of each token are summed
+ *           in registers, and each token's sum is added once at its hashed
+ *           addresses (float atomics; a token whose lookups span several
+ *           wavefronts adds one partial sum per wavefront).
+ * Both variants compute the same G; float summation order is not fixed. */
 enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2 };
 #define PSS_BWD_MASK 3u
 

@@ -15,7 +15,9 @@ namespace {
 
 using pss::KParams;
 
-constexpr uint64_t kMaxBags = 1ull << 38;
+// Bags and items are indexed with 32-bit integers in the sorted deposit.
+constexpr uint64_t kMaxBags = (1ull << 32) - 1;
+constexpr int64_t kMaxItems = (1ll << 32) - 1;
 
 int check_common(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) {
   if (hp == nullptr) return PSS_ERR_INVALID_ARG;
@@ -29,7 +31,7 @@ int check_common(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) {
   if (bags > kMaxBags) return PSS_ERR_INVALID_ARG;
   const uint64_t TC = static_cast<uint64_t>(hp->num_tables) * static_cast<uint64_t>(d / Z);
   if (TC >= (1ull << 32)) return PSS_ERR_INVALID_ARG;
-  if (hp->num_indices < 0) return PSS_ERR_INVALID_ARG;
+  if (hp->num_indices < 0 || hp->num_indices > kMaxItems) return PSS_ERR_INVALID_ARG;
   if (hp->weight_dtype != PSS_F32 && hp->weight_dtype != PSS_BF16) return PSS_ERR_UNSUPPORTED;
   if (hp->flags & ~PSS_BWD_MASK) return PSS_ERR_INVALID_ARG;
   return PSS_OK;
@@ -142,27 +144,35 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (state != nullptr && !(hash_params->eps >= 0.f && isfinite(hash_params->eps)))
     return PSS_ERR_INVALID_ARG;
   const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
-  if (variant == PSS_BWD_SORTED) return PSS_ERR_UNSUPPORTED;
   if (variant == 3) return PSS_ERR_INVALID_ARG;
+  const bool sorted = variant != PSS_BWD_ATOMIC;  // AUTO and SORTED
 
   const KParams p = make_params(M, Z, d, hash_params);
   const bool bf16 = hash_params->weight_dtype == PSS_BF16;
   if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
 
-  if (state == nullptr && !bf16) {
-    // SGD on float32 storage is linear in G: deposit -lr * grad directly.
-    return hip_status(pss::launch_deposit_atomic(static_cast<float*>(shared), -lr, p, indices,
-                                                 offsets, grad_out, stream));
+  // SGD on float32 storage is linear in G: deposit -lr * grad directly into
+  // the shared array.  Otherwise deposit G into a scratch buffer first.
+  const bool fused = state == nullptr && !bf16;
+  const size_t g_bytes = fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
+  const size_t ws_bytes = sorted ? pss::sorted_workspace_bytes(p.N) : 0;
+  void* ws = nullptr;
+  if (g_bytes + ws_bytes > 0) {
+    st = scratch_alloc(&ws, g_bytes + ws_bytes, stream);
+    if (st != PSS_OK) return st;
   }
-  void* G = nullptr;
-  st = scratch_alloc(&G, static_cast<size_t>(M) * sizeof(float), stream);
-  if (st != PSS_OK) return st;
-  float* Gf = static_cast<float*>(G);
-  hipError_t e = pss::launch_zero(Gf, M, stream);
-  if (e == hipSuccess) e = pss::launch_deposit_atomic(Gf, 1.f, p, indices, offsets, grad_out, stream);
-  if (e == hipSuccess)
-    e = pss::launch_optimizer(shared, bf16, state, Gf, M, lr, hash_params->eps, stream);
-  const hipError_t ef = hipFreeAsync(G, stream);
+  float* dst = fused ? static_cast<float*>(shared) : static_cast<float*>(ws);
+  void* sort_ws = static_cast<char*>(ws) + g_bytes;
+  const float scale = fused ? -lr : 1.f;
+  hipError_t e = hipSuccess;
+  if (!fused) e = pss::launch_zero(dst, M, stream);
+  if (e == hipSuccess) {
+    e = sorted ? pss::launch_deposit_sorted(dst, scale, p, indices, offsets, grad_out, sort_ws, stream)
+               : pss::launch_deposit_atomic(dst, scale, p, indices, offsets, grad_out, stream);
+  }
+  if (e == hipSuccess && !fused)
+    e = pss::launch_optimizer(shared, bf16, state, dst, M, lr, hash_params->eps, stream);
+  const hipError_t ef = ws ? hipFreeAsync(ws, stream) : hipSuccess;
   if (e != hipSuccess || ef != hipSuccess) return PSS_ERR_HIP;
   return PSS_OK;
 }

@@ -16,6 +16,14 @@ hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const int6
 hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, const int64_t* indices,
                                  const int64_t* offsets, const float* grad, hipStream_t stream);
 
+// Sorted deposit: lookups grouped by token (radix sort on the item hash),
+// gradient rows summed per token, one deposit of scale * sum per token and
+// wavefront.  `workspace` must hold sorted_workspace_bytes(p.N) bytes.
+size_t sorted_workspace_bytes(int64_t N);
+hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const int64_t* indices,
+                                 const int64_t* offsets, const float* grad, void* workspace,
+                                 hipStream_t stream);
+
 // Dense optimizer pass over the M elements of a gradient buffer G (G[m] == 0
 // leaves element m untouched).  state == nullptr selects SGD.
 hipError_t launch_optimizer(void* w, bool bf16, float* state, const float* G, int64_t M, float lr,

@@ -1,0 +1,308 @@
+// Sorted backward: group lookups by token, reduce, deposit once per token.
+//
+// Alg. 1's sparse branch (unique locations + scatter_add of the values onto
+// them) made hardware-friendly.  Identical tokens of a table read identical
+// chunk addresses, so their output-gradient rows can be summed first and the
+// sum deposited once: with the skewed token frequencies of recommendation
+// data this removes most of the deposits (and all of the hot spots).
+//
+//   keygen    item e -> (h0, r): h0 = item part of the hash (a * key0 + b
+//             mod p, identical for identical tokens, 31 bits), r = b*T + t
+//             the pooled row its gradient is read from.
+//   sort      LSD radix sort of the (h0, r) pairs by h0, 8-bit digits,
+//             stable; per pass a histogram kernel, one exclusive scan and a
+//             scatter kernel whose per-wave ranks come from ballot matching
+//             (no LDS atomics on the data path).
+//   reduce    one wavefront per 64 consecutive sorted pairs: accumulate the
+//             gradient rows of each run of equal h0 in registers (lanes over
+//             the dims), then add the run's sum at the run's hashed
+//             addresses with float atomics.  A token spanning several
+//             wavefronts deposits one partial sum per wavefront.
+#include "pss_launch.hpp"
+
+namespace pss {
+
+constexpr int kSortBits = 8;
+constexpr int kBins = 1 << kSortBits;
+constexpr int kSortItemsPerLane = 16;
+constexpr int kSortTile = kBlockThreads * kSortItemsPerLane;  // keys per block
+constexpr int kWaveSortKeys = kWave * kSortItemsPerLane;       // keys per wave
+
+// ---------------------------------------------------------------------------
+// keygen
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlockThreads) void keygen_kernel(
+    const KParams p, const int64_t* __restrict__ indices, const int64_t* __restrict__ offsets,
+    uint32_t* __restrict__ keys, uint32_t* __restrict__ rows) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+  const uint64_t g0 = wave * kTileBags;
+  if (g0 >= p.num_bags) return;
+  const Tile tl = load_tile(p, offsets, g0, lane);
+  // pooled row index r = b*T + t of bag g0 + lane
+  const uint64_t g = g0 + static_cast<uint64_t>(lane < tl.nb ? lane : 0);
+  const uint32_t t = static_cast<uint32_t>(g / p.B);
+  const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
+  const uint32_t rr = b * p.T + t;
+  for (int64_t blk = tl.E0; blk < tl.E1; blk += kWave) {
+    const int64_t rem = tl.E1 - blk;
+    const int n = rem < kWave ? static_cast<int>(rem) : kWave;
+    const int64_t e = blk + lane;
+    const int bag = bag_of_item(tl, e);
+    const uint32_t tC = __shfl(tl.tC, bag);
+    const uint32_t r = __shfl(rr, bag);
+    if (lane < n) {
+      const uint32_t i = static_cast<uint32_t>(__builtin_nontemporal_load(indices + e));
+      keys[e] = item_hash(i, tC, p.TC, p.a, p.b);
+      rows[e] = r;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// radix sort pieces
+// ---------------------------------------------------------------------------
+
+// Lanes holding the same digit as this lane (among lanes with `valid`).
+__device__ __forceinline__ uint64_t match_digit(uint32_t digit, bool valid) {
+  uint64_t eq = __ballot(valid);
+#pragma unroll
+  for (int bit = 0; bit < kSortBits; ++bit) {
+    const uint64_t m = __ballot((digit >> bit) & 1u);
+    eq &= ((digit >> bit) & 1u) ? m : ~m;
+  }
+  return eq;
+}
+
+__device__ __forceinline__ uint64_t lanes_below(int lane) {
+  return lane == 0 ? 0ull : (~0ull >> (kWave - lane));
+}
+
+// counts[d * nblocks + blk] = number of keys of tile blk with digit d.
+__global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
+    const uint32_t* __restrict__ keys, const int64_t n, const int shift,
+    uint32_t* __restrict__ counts, const uint32_t nblocks) {
+  __shared__ uint32_t hist[kWavesPerBlock][kBins];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
+  __syncthreads();
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile + w * kWaveSortKeys;
+#pragma unroll 4
+  for (int s = 0; s < kSortItemsPerLane; ++s) {
+    const int64_t idx = base + s * kWave + lane;
+    const bool valid = idx < n;
+    const uint32_t digit = valid ? (keys[idx] >> shift) & (kBins - 1) : 0u;
+    const uint64_t eq = match_digit(digit, valid);
+    // the lowest lane of each group adds the group's size (wave-private row)
+    if (valid && (eq & lanes_below(lane)) == 0) hist[w][digit] += __popcll(eq);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
+    uint32_t s = 0;
+#pragma unroll
+    for (int ww = 0; ww < kWavesPerBlock; ++ww) s += hist[ww][d];
+    counts[static_cast<uint64_t>(d) * nblocks + blockIdx.x] = s;
+  }
+}
+
+// In-place exclusive scan of counts[0 .. len) by a single workgroup.
+__global__ __launch_bounds__(1024) void sort_scan_kernel(uint32_t* __restrict__ counts,
+                                                         const uint64_t len) {
+  __shared__ uint32_t part[1024];
+  const uint64_t per = (len + 1023) / 1024;
+  const uint64_t lo = threadIdx.x * per;
+  const uint64_t hi = lo + per < len ? lo + per : len;
+  uint32_t s = 0;
+  for (uint64_t i = lo; i < hi; ++i) s += counts[i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  // Hillis-Steele inclusive scan of the 1024 partial sums
+  for (int off = 1; off < 1024; off <<= 1) {
+    const uint32_t v = threadIdx.x >= static_cast<unsigned>(off) ? part[threadIdx.x - off] : 0u;
+    __syncthreads();
+    part[threadIdx.x] += v;
+    __syncthreads();
+  }
+  uint32_t run = threadIdx.x == 0 ? 0u : part[threadIdx.x - 1];
+  for (uint64_t i = lo; i < hi; ++i) {
+    const uint32_t c = counts[i];
+    counts[i] = run;
+    run += c;
+  }
+}
+
+// Stable scatter of one tile by digit into its global slots.
+__global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
+    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, const int64_t n,
+    const int shift, const uint32_t* __restrict__ offsets, const uint32_t nblocks) {
+  __shared__ uint32_t cur[kWavesPerBlock][kBins];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&cur[0][0])[i] = 0;
+  __syncthreads();
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile + w * kWaveSortKeys;
+  uint32_t k[kSortItemsPerLane], v[kSortItemsPerLane];
+#pragma unroll
+  for (int s = 0; s < kSortItemsPerLane; ++s) {
+    const int64_t idx = base + s * kWave + lane;
+    k[s] = idx < n ? keys_in[idx] : 0u;
+    v[s] = idx < n ? vals_in[idx] : 0u;
+  }
+  // per-wave digit counts
+#pragma unroll
+  for (int s = 0; s < kSortItemsPerLane; ++s) {
+    const bool valid = base + s * kWave + lane < n;
+    const uint32_t digit = (k[s] >> shift) & (kBins - 1);
+    const uint64_t eq = match_digit(digit, valid);
+    if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
+  }
+  __syncthreads();
+  // wave start offsets: global slot of the tile + counts of earlier waves
+  for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
+    uint32_t run = offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
+#pragma unroll
+    for (int ww = 0; ww < kWavesPerBlock; ++ww) {
+      const uint32_t c = cur[ww][d];
+      cur[ww][d] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < kSortItemsPerLane; ++s) {
+    const bool valid = base + s * kWave + lane < n;
+    const uint32_t digit = (k[s] >> shift) & (kBins - 1);
+    const uint64_t eq = match_digit(digit, valid);
+    const uint32_t pos = cur[w][digit] + static_cast<uint32_t>(__popcll(eq & lanes_below(lane)));
+    if (valid && pos < n) {  // always true when the counts agree; guards memory anyway
+      keys_out[pos] = k[s];
+      vals_out[pos] = v[s];
+    }
+    // all lanes have read cur[w][digit] above; group leaders advance it
+    if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// segmented reduction + deposit
+// ---------------------------------------------------------------------------
+template <int EPL, int U>
+__global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
+    float* __restrict__ dst, const float scale, const KParams p,
+    const uint32_t* __restrict__ keys, const uint32_t* __restrict__ rows,
+    const float* __restrict__ grad, const int64_t n) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6)) * kWave;
+  if (p0 >= n) return;
+  const int cnt = n - p0 < kWave ? static_cast<int>(n - p0) : kWave;
+  const uint32_t c0 = blockIdx.y * (kWave * EPL);
+
+  uint32_t step[EPL], kk[EPL];
+  bool act[EPL];
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) {
+    const uint32_t c = c0 + lane + kWave * r;
+    act[r] = c < p.d;
+    const uint32_t cc = act[r] ? c : 0;
+    const uint32_t j = cc / p.Z;
+    kk[r] = cc - j * p.Z;
+    step[r] = chunk_step(p.a, j);
+  }
+  uint32_t key = 0xffffffffu, row = 0;
+  if (lane < cnt) {
+    key = keys[p0 + lane];
+    row = rows[p0 + lane];
+    if (row >= p.num_bags) row = 0;  // rows come from keygen; clamp keeps reads in bounds
+  }
+  float acc[EPL];
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
+
+  for (int q = 0; q < cnt; q += U) {
+    float gv[U][EPL];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (q + u < cnt) {
+        const float* grow = grad + static_cast<uint64_t>(readlane_u32(row, q + u)) * p.d + c0 + lane;
+#pragma unroll
+        for (int r = 0; r < EPL; ++r) gv[u][r] = act[r] ? __builtin_nontemporal_load(grow + kWave * r) : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (q + u < cnt) {
+#pragma unroll
+        for (int r = 0; r < EPL; ++r) acc[r] += gv[u][r];
+        const uint32_t h = readlane_u32(key, q + u);
+        const uint32_t hn = q + u + 1 < cnt ? readlane_u32(key, q + u + 1) : ~h;
+        if (hn != h) {
+#pragma unroll
+          for (int r = 0; r < EPL; ++r) {
+            if (act[r]) {
+              const uint32_t base = fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M);
+              unsafeAtomicAdd(dst + wrap_add(base, kk[r], p.M), scale * acc[r]);
+            }
+            acc[r] = 0.f;
+          }
+        }
+      }
+    }
+  }
+}
+
+size_t sorted_workspace_bytes(int64_t N) {
+  const uint64_t nblocks = (static_cast<uint64_t>(N) + kSortTile - 1) / kSortTile;
+  return static_cast<size_t>(N) * 16 + nblocks * kBins * 4 + 256;
+}
+
+template <int EPL, int U>
+static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, const uint32_t* keys,
+                                  const uint32_t* rows, const float* grad, hipStream_t stream) {
+  const uint64_t waves = (static_cast<uint64_t>(p.N) + kWave - 1) / kWave;
+  const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+  const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
+  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U>), dim3(static_cast<uint32_t>(blocks), slabs),
+                     dim3(kBlockThreads), 0, stream, dst, scale, p, keys, rows, grad, p.N);
+  return hipGetLastError();
+}
+
+hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const int64_t* indices,
+                                 const int64_t* offsets, const float* grad, void* workspace,
+                                 hipStream_t stream) {
+  const int64_t N = p.N;
+  if (N == 0) return hipSuccess;
+  uint32_t* k0 = static_cast<uint32_t*>(workspace);
+  uint32_t* v0 = k0 + N;
+  uint32_t* k1 = v0 + N;
+  uint32_t* v1 = k1 + N;
+  uint32_t* counts = v1 + N;
+  const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
+
+  {
+    const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
+    const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL(keygen_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kBlockThreads), 0,
+                       stream, p, indices, offsets, k0, v0);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // h0 < 2^31: four 8-bit passes, ping-pong between the two buffers
+  for (int shift = 0; shift < 31; shift += kSortBits) {
+    hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, N,
+                       shift, counts, nblocks);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(1), dim3(1024), 0, stream, counts,
+                       static_cast<uint64_t>(nblocks) * kBins);
+    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, v0,
+                       k1, v1, N, shift, counts, nblocks);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    uint32_t* t = k0; k0 = k1; k1 = t;
+    t = v0; v0 = v1; v1 = t;
+  }
+  if (p.d <= 64) return launch_reduce_t<1, 16>(dst, scale, p, k0, v0, grad, stream);
+  if (p.d <= 128) return launch_reduce_t<2, 8>(dst, scale, p, k0, v0, grad, stream);
+  if (p.d <= 256) return launch_reduce_t<4, 4>(dst, scale, p, k0, v0, grad, stream);
+  return launch_reduce_t<8, 2>(dst, scale, p, k0, v0, grad, stream);
+}
+
+}  // namespace pss

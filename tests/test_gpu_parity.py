@@ -21,6 +21,9 @@ CASES = [("c1", None, None), ("c2", 700, None), ("c3", 50, None), ("c4", 300, 50
          ("c5", 900, None)]
 
 
+VARIANTS = {"atomic": pss.PSS_BWD_ATOMIC, "sorted": pss.PSS_BWD_SORTED}
+
+
 def _id(c):
     return f"{c[0]}-B{c[1]}"
 
@@ -75,10 +78,11 @@ def test_forward_parity(case):
     parity.check_forward(got, ref, s_abs, 1e-5)
 
 
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
 @pytest.mark.parametrize("case", CASES, ids=_id)
-def test_backward_update_parity(case):
+def test_backward_update_parity(case, variant):
     key, B, M = case
-    L = Layer(synth.get(key), B=B, M=M)
+    L = Layer(synth.get(key), B=B, M=M, flags=VARIANTS[variant])
     g = synth.make_grad(L.wl, B=L.B)
     L.backward(g)
     w_ref, s_ref, G, A, cnt = L.ref_backward(g)
@@ -86,10 +90,11 @@ def test_backward_update_parity(case):
     parity.check_update(L, L.weights(), s_gpu, w_ref, s_ref, G, A, L.wl.lr)
 
 
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
 @pytest.mark.parametrize("key", ["c3", "c5"])
-def test_adagrad_warm_state(key):
+def test_adagrad_warm_state(key, variant):
     """Adagrad from s0 = 0.1: well conditioned everywhere, no exemptions."""
-    L = Layer(synth.get(key), B=40, s0=0.1)
+    L = Layer(synth.get(key), B=40, s0=0.1, flags=VARIANTS[variant])
     g = synth.make_grad(L.wl, B=L.B)
     L.backward(g)
     w_ref, s_ref, G, A, _ = L.ref_backward(g)
@@ -97,25 +102,27 @@ def test_adagrad_warm_state(key):
     assert ex == 0
 
 
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
 @pytest.mark.parametrize("key,M,Z,d", [("c1", 4096, 4, 16), ("c1", 97, 8, 24), ("c3", 1000, 16, 64),
                                        ("c1", 300, 1, 7), ("c5", 5000, 128, 128)])
-def test_unit_gradient_counts_bit_exact(key, M, Z, d):
+def test_unit_gradient_counts_bit_exact(key, M, Z, d, variant):
     """grad_out = 1, w = 0, lr = 1 ("loss = sum of retrieved elements"):
     w_new[m] = -(number of reads of m), an exact integer, wrap included."""
     wl = synth.get(key).scaled(M=M, Z=Z, d=d, optimizer="sgd", weight_dtype="f32")
-    L = Layer(wl, B=150, w=np.zeros(M, dtype=np.float32))
+    L = Layer(wl, B=150, w=np.zeros(M, dtype=np.float32), flags=VARIANTS[variant])
     ones = np.ones((L.B, wl.T * wl.d), dtype=np.float32)
     L.backward(ones, lr=1.0)
     _, _, _, _, cnt = L.ref_backward(ones, lr=1.0)
     assert np.array_equal(L.weights(), -cnt.astype(np.float32))
 
 
-def test_gradient_mass_per_chunk_offset():
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
+def test_gradient_mass_per_chunk_offset(variant):
     """Masking grad_out to columns c with c mod Z = k moves exactly
     lr * (masked gradient mass) out of the array, for every k."""
     wl = synth.get("c1")
     for k in range(wl.Z):
-        L = Layer(wl, B=256)
+        L = Layer(wl, B=256, flags=VARIANTS[variant])
         g = synth.make_grad(wl, B=L.B)
         cols = (np.arange(wl.T * wl.d) % wl.d) % wl.Z == k
         gk = np.where(cols[None, :], g, 0).astype(np.float32)
@@ -142,11 +149,12 @@ EDGE = [
 ]
 
 
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
 @pytest.mark.parametrize("name,over,B", EDGE, ids=[e[0] for e in EDGE])
 @pytest.mark.parametrize("opt", ["sgd", "adagrad"])
-def test_edge_shapes(name, over, B, opt):
+def test_edge_shapes(name, over, B, opt, variant):
     wl = synth.get("c1").scaled(optimizer=opt, lr=0.05, **over)
-    L = Layer(wl, B=B)
+    L = Layer(wl, B=B, flags=VARIANTS[variant])
     got = L.forward()
     ref, s_abs = L.ref_forward()
     parity.check_forward(got, ref, s_abs, 1e-5)
@@ -159,11 +167,31 @@ def test_edge_shapes(name, over, B, opt):
     parity.check_update(L, L.weights(), s_gpu, w_ref, s_ref, G, A, wl.lr)
 
 
-def test_bf16_sgd_storage():
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
+def test_bf16_sgd_storage(variant):
     """bf16 storage with SGD goes through the gradient buffer and rounds once."""
     wl = synth.get("c5").scaled(optimizer="sgd", lr=0.1, M=300_000)
-    L = Layer(wl, B=500)
+    L = Layer(wl, B=500, flags=VARIANTS[variant])
     g = synth.make_grad(wl, B=L.B)
     L.backward(g)
     w_ref, _, G, A, _ = L.ref_backward(g)
     parity.check_update(L, L.weights(), None, w_ref, None, G, A, wl.lr)
+
+
+@pytest.mark.parametrize("key", ["c2", "c3"])
+def test_sorted_and_atomic_agree(key):
+    """Alg. 1's two branches compute the same gradient: the sorted (unique
+    tokens, summed) and the per-contribution atomic deposits agree to the
+    normalised tolerance element by element."""
+    wl = synth.get(key).scaled(optimizer="adagrad", lr=0.01)
+    La = Layer(wl, B=200, flags=pss.PSS_BWD_ATOMIC, s0=0.1)
+    Ls = Layer(wl, B=200, flags=pss.PSS_BWD_SORTED, s0=0.1)
+    g = synth.make_grad(wl, B=200)
+    La.backward(g)
+    Ls.backward(g)
+    _, s_ref, G, A, _ = La.ref_backward(g)
+    sa = La.state.cpu().numpy().astype(np.float64)
+    ss = Ls.state.cpu().numpy().astype(np.float64)
+    bound = 1e-5 * (0.1 + A * A) + 1e-30
+    assert np.all(np.abs(sa - ss) <= 2 * bound)
+    assert np.all(np.abs(ss - s_ref) <= bound)

@@ -9,11 +9,13 @@
 //   keygen    item e -> (h0, r): h0 = item part of the hash (a * key0 + b
 //             mod p, identical for identical tokens, 31 bits), r = b*T + t
 //             the pooled row its gradient is read from.
-//   sort      LSD radix sort of the (h0, r) pairs by h0, 8-bit digits,
-//             stable; per pass a histogram kernel, one exclusive scan and a
-//             scatter kernel whose per-wave ranks come from ballot matching
-//             (no LDS atomics on the data path).
-//   reduce    one wavefront per 64 consecutive sorted pairs: accumulate the
+//   sort      LSD radix sort of the (h0, r) pairs on the low 8, 16 or 24
+//             bits of h0 (groups of about 32 pairs), 8-bit digits, stable;
+//             per pass a histogram kernel, a per-digit scan (one workgroup
+//             per digit) and a scatter kernel whose per-wave ranks come from
+//             ballot matching (no atomics on the data path).
+//   reduce    one wavefront per 64 consecutive sorted pairs: sort them by
+//             the full h0 (bitonic network over the lanes), accumulate the
 //             gradient rows of each run of equal h0 in registers (lanes over
 //             the dims), then add the run's sum at the run's hashed
 //             addresses with float atomics.  A token spanning several
@@ -27,6 +29,7 @@ constexpr int kBins = 1 << kSortBits;
 constexpr int kSortItemsPerLane = 16;
 constexpr int kSortTile = kBlockThreads * kSortItemsPerLane;  // keys per block
 constexpr int kWaveSortKeys = kWave * kSortItemsPerLane;       // keys per wave
+static_assert(kBins == kBlockThreads, "one digit per thread in the scatter prologue");
 
 // ---------------------------------------------------------------------------
 // keygen
@@ -105,38 +108,56 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
   }
 }
 
-// In-place exclusive scan of counts[0 .. len) by a single workgroup.
-__global__ __launch_bounds__(1024) void sort_scan_kernel(uint32_t* __restrict__ counts,
-                                                         const uint64_t len) {
-  __shared__ uint32_t part[1024];
-  const uint64_t per = (len + 1023) / 1024;
-  const uint64_t lo = threadIdx.x * per;
-  const uint64_t hi = lo + per < len ? lo + per : len;
-  uint32_t s = 0;
-  for (uint64_t i = lo; i < hi; ++i) s += counts[i];
-  part[threadIdx.x] = s;
+// Exclusive scan over the 256 threads of a block (wave scans + LDS carry).
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum,
+                                                         uint32_t* total) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == kWave - 1) wsum[w] = x;
   __syncthreads();
-  // Hillis-Steele inclusive scan of the 1024 partial sums
-  for (int off = 1; off < 1024; off <<= 1) {
-    const uint32_t v = threadIdx.x >= static_cast<unsigned>(off) ? part[threadIdx.x - off] : 0u;
-    __syncthreads();
-    part[threadIdx.x] += v;
-    __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int ww = 0; ww < kWavesPerBlock; ++ww) {
+    before += ww < w ? wsum[ww] : 0u;
+    all += wsum[ww];
   }
-  uint32_t run = threadIdx.x == 0 ? 0u : part[threadIdx.x - 1];
-  for (uint64_t i = lo; i < hi; ++i) {
-    const uint32_t c = counts[i];
-    counts[i] = run;
-    run += c;
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
+// Row d of counts (one digit, nblocks entries): exclusive scan in place;
+// totals[d] = the row's sum.  One workgroup per digit.
+__global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __restrict__ counts,
+                                                                  const uint32_t nblocks,
+                                                                  uint32_t* __restrict__ totals) {
+  __shared__ uint32_t wsum[kWavesPerBlock];
+  uint32_t* row = counts + static_cast<uint64_t>(blockIdx.x) * nblocks;
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nblocks; base += kBlockThreads) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i < nblocks ? row[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(v, wsum, &tot);
+    if (i < nblocks) row[i] = carry + ex;
+    carry += tot;
   }
+  if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
 // Stable scatter of one tile by digit into its global slots.
 __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, const int64_t n,
-    const int shift, const uint32_t* __restrict__ offsets, const uint32_t nblocks) {
+    const int shift, const uint32_t* __restrict__ offsets, const uint32_t nblocks,
+    const uint32_t* __restrict__ totals) {
   __shared__ uint32_t cur[kWavesPerBlock][kBins];
+  __shared__ uint32_t wsum[kWavesPerBlock];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&cur[0][0])[i] = 0;
   __syncthreads();
@@ -156,10 +177,14 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint64_t eq = match_digit(digit, valid);
     if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
   }
+  // first slot of each digit: exclusive scan of the digit totals (one digit
+  // per thread)
+  uint32_t unused;
+  const uint32_t digit_base = block_exclusive_scan(totals[threadIdx.x], wsum, &unused);
   __syncthreads();
   // wave start offsets: global slot of the tile + counts of earlier waves
   for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
-    uint32_t run = offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
+    uint32_t run = digit_base + offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
 #pragma unroll
     for (int ww = 0; ww < kWavesPerBlock; ++ww) {
       const uint32_t c = cur[ww][d];
@@ -214,6 +239,26 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
     row = rows[p0 + lane];
     if (row >= p.num_bags) row = 0;  // rows come from keygen; clamp keeps reads in bounds
   }
+  // Bitonic sort of the wave's 64 (key, row) pairs by the full key: the
+  // global sort only orders the low bits, so tokens that share them can
+  // arrive interleaved; sorted, each token of the piece forms one run.
+  // Empty lanes hold key 0xffffffff (> any hash) and stay at the end.
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint32_t ok = __shfl_xor(key, j);
+      const uint32_t orow = __shfl_xor(row, j);
+      const bool up = (lane & k) == 0;
+      const bool lower = (lane & j) == 0;
+      // the lower lane of an ascending pair keeps the smaller key
+      const bool take = lower == up ? ok < key : ok > key;
+      if (take) {
+        key = ok;
+        row = orow;
+      }
+    }
+  }
   float acc[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
@@ -252,7 +297,7 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
 
 size_t sorted_workspace_bytes(int64_t N) {
   const uint64_t nblocks = (static_cast<uint64_t>(N) + kSortTile - 1) / kSortTile;
-  return static_cast<size_t>(N) * 16 + nblocks * kBins * 4 + 256;
+  return static_cast<size_t>(N) * 16 + nblocks * kBins * 4 + kBins * 4 + 256;
 }
 
 template <int EPL, int U>
@@ -276,6 +321,7 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   uint32_t* k1 = v0 + N;
   uint32_t* v1 = k1 + N;
   uint32_t* counts = v1 + N;
+  uint32_t* totals = counts + static_cast<uint64_t>((N + kSortTile - 1) / kSortTile) * kBins;
   const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
 
   {
@@ -286,14 +332,19 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // h0 < 2^31: four 8-bit passes, ping-pong between the two buffers
-  for (int shift = 0; shift < 31; shift += kSortBits) {
+  // Grouping only needs equal keys close together: sort by the low bits of
+  // h0, enough of them that a group of equal low bits holds about 32 pairs
+  // on average; the reduction's in-register sort then separates the tokens
+  // of a group.  Whole 8-bit passes, at most 24 bits, ping-pong buffers.
+  int bits = kSortBits;
+  while (bits < 24 && (static_cast<int64_t>(32) << bits) < N) bits += kSortBits;
+  for (int shift = 0; shift < bits; shift += kSortBits) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, N,
                        shift, counts, nblocks);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(1), dim3(1024), 0, stream, counts,
-                       static_cast<uint64_t>(nblocks) * kBins);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
+                       nblocks, totals);
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, v0,
-                       k1, v1, N, shift, counts, nblocks);
+                       k1, v1, N, shift, counts, nblocks, totals);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     uint32_t* t = k0; k0 = k1; k1 = t;

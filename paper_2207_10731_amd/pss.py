@@ -15,7 +15,8 @@ import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libpss.so")
-HEADER = os.path.join(os.path.dirname(_PKG), "include", "pss.h")
+INCLUDE = os.path.join(os.path.dirname(_PKG), "include")
+HEADER = os.path.join(INCLUDE, "pss.h")
 
 PSS_PRIME = 2**31 - 1
 PSS_F32, PSS_BF16 = 0, 1
@@ -70,12 +71,17 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
-def header_functions(path: str = HEADER) -> list[str]:
-    """Names of the functions declared in include/pss.h."""
-    with open(path) as f:
-        text = f.read()
-    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)  # drop comments
-    return sorted(set(re.findall(r"\b(pss_\w+)\s*\(", text)))
+def header_functions(paths=None) -> list[str]:
+    """Names of the functions declared in the headers (default: include/*.h)."""
+    if paths is None:
+        paths = sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
+    names = set()
+    for path in paths:
+        with open(path) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)  # drop comments
+        names.update(re.findall(r"\b(pss_\w+)\s*\(", text))
+    return sorted(names)
 
 
 def status_string(status: int) -> str:

@@ -20,7 +20,7 @@ __device__ __forceinline__ uint64_t readlane_u64b(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-template <int EPL, int U>
+template <int EPL, int U, bool TAB>
 __global__ __launch_bounds__(kBlockThreads) void deposit_kernel(
     float* __restrict__ dst, const float scale, const KParams p,
     const int64_t* __restrict__ indices, const int64_t* __restrict__ offsets,
@@ -30,17 +30,19 @@ __global__ __launch_bounds__(kBlockThreads) void deposit_kernel(
   const uint64_t g0 = wave * kTileBags;
   if (g0 >= p.num_bags) return;
   const uint32_t c0 = blockIdx.y * (kWave * EPL);
+  __shared__ uint32_t tab_all[TAB ? kWavesPerBlock * kWave * kTabStride : 1];
+  uint32_t* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabStride : 0);
 
-  uint32_t step[EPL], kk[EPL];
+  uint32_t step[EPL], kk[EPL], jj[EPL];
   bool act[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) {
     const uint32_t c = c0 + lane + kWave * r;
     act[r] = c < p.d;
     const uint32_t cc = act[r] ? c : 0;
-    const uint32_t j = cc / p.Z;
-    kk[r] = cc - j * p.Z;
-    step[r] = chunk_step(p.a, j);
+    jj[r] = cc / p.Z;
+    kk[r] = cc - jj[r] * p.Z;
+    step[r] = TAB ? 0u : chunk_step(p.a, jj[r]);
   }
 
   const Tile tl = load_tile(p, offsets, g0, lane);
@@ -54,6 +56,7 @@ __global__ __launch_bounds__(kBlockThreads) void deposit_kernel(
     const int bag = bag_of_item(tl, e);
     const uint32_t tC = __shfl(tl.tC, bag);
     const uint64_t ro = __shfl(tl.row_off, bag);
+    if (TAB) fill_base_table(tab, item_hash(idx, tC, p.TC, p.a, p.b), p, lane);
 
     for (int q = 0; q < n; q += U) {
       float gv[U][EPL];
@@ -62,15 +65,17 @@ __global__ __launch_bounds__(kBlockThreads) void deposit_kernel(
       for (int u = 0; u < U; ++u) {
         if (q + u < n) {
           const float* grow = grad + readlane_u64b(ro, q + u) + c0 + lane;
-          const uint32_t h0 = item_hash(readlane_u32(idx, q + u), readlane_u32(tC, q + u), p.TC,
-                                        p.a, p.b);
+          uint32_t h0 = 0;
+          if (!TAB)
+            h0 = item_hash(readlane_u32(idx, q + u), readlane_u32(tC, q + u), p.TC, p.a, p.b);
 #pragma unroll
           for (int r = 0; r < EPL; ++r) {
             gv[u][r] = 0.f;
             m[u][r] = 0;
             if (act[r]) {
               gv[u][r] = __builtin_nontemporal_load(grow + kWave * r);
-              const uint32_t base = fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M);
+              const uint32_t base = TAB ? tab[(q + u) * kTabStride + jj[r]]
+                                        : fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M);
               m[u][r] = wrap_add(base, kk[r], p.M);
             }
           }
@@ -88,7 +93,7 @@ __global__ __launch_bounds__(kBlockThreads) void deposit_kernel(
   }
 }
 
-template <int EPL, int U>
+template <int EPL, int U, bool TAB>
 static hipError_t launch_dep_t(float* dst, float scale, const KParams& p, const int64_t* indices,
                                const int64_t* offsets, const float* grad, hipStream_t stream) {
   const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
@@ -96,17 +101,25 @@ static hipError_t launch_dep_t(float* dst, float scale, const KParams& p, const 
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
   if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
   dim3 grid(static_cast<uint32_t>(blocks), slabs);
-  hipLaunchKernelGGL((deposit_kernel<EPL, U>), grid, dim3(kBlockThreads), 0, stream, dst, scale,
+  hipLaunchKernelGGL((deposit_kernel<EPL, U, TAB>), grid, dim3(kBlockThreads), 0, stream, dst, scale,
                      p, indices, offsets, grad);
   return hipGetLastError();
 }
 
+template <bool TAB>
+static hipError_t launch_dep_c(float* dst, float scale, const KParams& p, const int64_t* indices,
+                               const int64_t* offsets, const float* grad, hipStream_t stream) {
+  if (p.d <= 64) return launch_dep_t<1, 16, TAB>(dst, scale, p, indices, offsets, grad, stream);
+  if (p.d <= 128) return launch_dep_t<2, 8, TAB>(dst, scale, p, indices, offsets, grad, stream);
+  if (p.d <= 256) return launch_dep_t<4, 4, TAB>(dst, scale, p, indices, offsets, grad, stream);
+  return launch_dep_t<8, 2, TAB>(dst, scale, p, indices, offsets, grad, stream);
+}
+
 hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, const int64_t* indices,
                                  const int64_t* offsets, const float* grad, hipStream_t stream) {
-  if (p.d <= 64) return launch_dep_t<1, 16>(dst, scale, p, indices, offsets, grad, stream);
-  if (p.d <= 128) return launch_dep_t<2, 8>(dst, scale, p, indices, offsets, grad, stream);
-  if (p.d <= 256) return launch_dep_t<4, 4>(dst, scale, p, indices, offsets, grad, stream);
-  return launch_dep_t<8, 2>(dst, scale, p, indices, offsets, grad, stream);
+  if (p.C <= static_cast<uint32_t>(kTabChunks))
+    return launch_dep_c<true>(dst, scale, p, indices, offsets, grad, stream);
+  return launch_dep_c<false>(dst, scale, p, indices, offsets, grad, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -1,13 +1,17 @@
 // Forward of the PSS layer: hash -> chunk gather -> sum-pool (paper Sec. 2.4
 // forward(i) = (S e_i)^T M with the ROBE-Z mapping of Sec. 2.5).
 //
-// One wavefront per tile of 64 bags.  For each item the hash's item part is
-// evaluated once for the whole wave (scalar unit: the token index is read
-// from a lane with readlane), each lane adds its chunk's constant, reduces
-// mod M and reads its dims.  U items are gathered before any is consumed so
+// One wavefront per tile of 64 bags.  Hashing: with C = d/Z <= 16 chunks,
+// each lane evaluates the C chunk bases of one item of the current 64-item
+// block into a wave-private LDS table and the gathers read their base from
+// it (one modular reduction per chunk instead of one per dim); with more
+// chunks each lane hashes its own dims (item part on the scalar unit).  U items are gathered before any is consumed so
 // that U * EPL loads per lane are in flight.  Pooling runs in registers in
 // item order; a finished bag's row is written with non-temporal stores (the
 // 4 bytes/dim output stream must not evict the shared array from L2/MALL).
+// On gfx9 stores and loads share one wait counter, so the kernel issues all
+// U gathers of a batch before any store of that batch: a store is never
+// followed by a wait for a load issued after it.
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -18,7 +22,7 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-template <typename WT, int EPL, int U>
+template <typename WT, int EPL, int U, bool TAB>
 __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     const WT* __restrict__ w, const KParams p, const int64_t* __restrict__ indices,
     const int64_t* __restrict__ offsets, float* __restrict__ out) {
@@ -28,16 +32,19 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
   if (g0 >= p.num_bags) return;
   const uint32_t c0 = blockIdx.y * (kWave * EPL);
 
-  uint32_t step[EPL], kk[EPL];
+  __shared__ uint32_t tab_all[TAB ? kWavesPerBlock * kWave * kTabStride : 1];
+  uint32_t* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabStride : 0);
+
+  uint32_t step[EPL], kk[EPL], jj[EPL];
   bool act[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) {
     const uint32_t c = c0 + lane + kWave * r;
     act[r] = c < p.d;
     const uint32_t cc = act[r] ? c : 0;
-    const uint32_t j = cc / p.Z;
-    kk[r] = cc - j * p.Z;
-    step[r] = chunk_step(p.a, j);
+    jj[r] = cc / p.Z;
+    kk[r] = cc - jj[r] * p.Z;
+    step[r] = TAB ? 0u : chunk_step(p.a, jj[r]);
   }
 
   const Tile tl = load_tile(p, offsets, g0, lane);
@@ -62,24 +69,28 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     if (lane < n) idx = static_cast<uint32_t>(__builtin_nontemporal_load(indices + e));
     const int bag = bag_of_item(tl, e);
     const uint32_t tC = __shfl(tl.tC, bag);
+    if (TAB) fill_base_table(tab, item_hash(idx, tC, p.TC, p.a, p.b), p, lane);
 
     for (int q = 0; q < n; q += U) {
+      // Gather phase: straight-line, U items x EPL loads in flight.  Items
+      // past the end of the block re-read the last item (clamped index) and
+      // inactive dims read element 0, so no load sits behind a branch.
       float v[U][EPL];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        if (q + u < n) {
-          const uint32_t i = readlane_u32(idx, q + u);
-          const uint32_t h0 = item_hash(i, readlane_u32(tC, q + u), p.TC, p.a, p.b);
+        const int uu = q + u < n ? q + u : n - 1;
+        uint32_t h0 = 0;
+        if (!TAB) h0 = item_hash(readlane_u32(idx, uu), readlane_u32(tC, uu), p.TC, p.a, p.b);
 #pragma unroll
-          for (int r = 0; r < EPL; ++r) {
-            v[u][r] = 0.f;
-            if (act[r]) {
-              const uint32_t base = fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M);
-              v[u][r] = load_weight(w, wrap_add(base, kk[r], p.M));
-            }
-          }
+        for (int r = 0; r < EPL; ++r) {
+          const uint32_t base = TAB ? tab[uu * kTabStride + jj[r]]
+                                    : fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M);
+          const uint32_t m = act[r] ? wrap_add(base, kk[r], p.M) : 0u;
+          v[u][r] = load_weight(w, m);
         }
       }
+      // Pool phase: stores only here, after every gather of the batch was
+      // issued (a store counts in the same wait counter as the gathers).
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         if (q + u < n) {
@@ -101,7 +112,7 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
   for (int z = cur + 1; z < tl.nb; ++z) store_row(z, true);
 }
 
-template <typename WT, int EPL, int U>
+template <typename WT, int EPL, int U, bool TAB>
 static hipError_t launch_fwd_t(const WT* w, const KParams& p, const int64_t* indices,
                                const int64_t* offsets, float* out, hipStream_t stream) {
   const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
@@ -109,18 +120,26 @@ static hipError_t launch_fwd_t(const WT* w, const KParams& p, const int64_t* ind
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
   if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
   dim3 grid(static_cast<uint32_t>(blocks), slabs);
-  hipLaunchKernelGGL((forward_kernel<WT, EPL, U>), grid, dim3(kBlockThreads), 0, stream, w, p,
+  hipLaunchKernelGGL((forward_kernel<WT, EPL, U, TAB>), grid, dim3(kBlockThreads), 0, stream, w, p,
                      indices, offsets, out);
   return hipGetLastError();
+}
+
+template <typename WT, bool TAB>
+static hipError_t launch_fwd_c(const WT* w, const KParams& p, const int64_t* indices,
+                               const int64_t* offsets, float* out, hipStream_t stream) {
+  if (p.d <= 64) return launch_fwd_t<WT, 1, 16, TAB>(w, p, indices, offsets, out, stream);
+  if (p.d <= 128) return launch_fwd_t<WT, 2, 8, TAB>(w, p, indices, offsets, out, stream);
+  if (p.d <= 256) return launch_fwd_t<WT, 4, 4, TAB>(w, p, indices, offsets, out, stream);
+  return launch_fwd_t<WT, 8, 2, TAB>(w, p, indices, offsets, out, stream);
 }
 
 template <typename WT>
 static hipError_t launch_fwd_w(const WT* w, const KParams& p, const int64_t* indices,
                                const int64_t* offsets, float* out, hipStream_t stream) {
-  if (p.d <= 64) return launch_fwd_t<WT, 1, 16>(w, p, indices, offsets, out, stream);
-  if (p.d <= 128) return launch_fwd_t<WT, 2, 8>(w, p, indices, offsets, out, stream);
-  if (p.d <= 256) return launch_fwd_t<WT, 4, 4>(w, p, indices, offsets, out, stream);
-  return launch_fwd_t<WT, 8, 2>(w, p, indices, offsets, out, stream);
+  if (p.C <= static_cast<uint32_t>(kTabChunks))
+    return launch_fwd_c<WT, true>(w, p, indices, offsets, out, stream);
+  return launch_fwd_c<WT, false>(w, p, indices, offsets, out, stream);
 }
 
 hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const int64_t* indices,

@@ -110,6 +110,23 @@ __device__ __forceinline__ Tile load_tile(const KParams& p, const int64_t* __res
   return tl;
 }
 
+// Chunk-base table.  For C = d/Z <= kTabChunks, lane l of a wavefront
+// evaluates the C chunk bases of item l of the current 64-item block once
+// (the modular reduction by M costs quarter-rate 64-bit multiplies) and keeps
+// them in a wave-private LDS table; every lane then reads the base of the
+// chunk it needs with a broadcast LDS read.  Wider C (small Z) hashes per lane.
+constexpr int kTabChunks = 16;
+constexpr int kTabStride = kTabChunks + 1;  // padding against bank conflicts
+
+__device__ __forceinline__ void fill_base_table(uint32_t* tab, uint32_t h0, const KParams& p,
+                                                int lane) {
+  uint32_t step = 0;  // a * j mod p, j = 0 .. C-1
+  for (uint32_t j = 0; j < p.C; ++j) {
+    tab[lane * kTabStride + j] = fast_mod(add_mod_p(h0, step), p.fm_c, p.M);
+    step = add_mod_p(step, p.a);
+  }
+}
+
 // Local bag (0..nb-1) of item e of the tile: the largest l with start[l] <= e.
 // Binary search over the starts held in the lanes (6 cross-lane reads).
 __device__ __forceinline__ int bag_of_item(const Tile& tl, int64_t e) {

@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
 // ---------------------------------------------------------------------------
 // segmented reduction + deposit
 // ---------------------------------------------------------------------------
-template <int EPL, int U>
+template <int EPL, int U, bool TAB>
 __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
     float* __restrict__ dst, const float scale, const KParams p,
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ rows,
@@ -221,17 +221,19 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
   if (p0 >= n) return;
   const int cnt = n - p0 < kWave ? static_cast<int>(n - p0) : kWave;
   const uint32_t c0 = blockIdx.y * (kWave * EPL);
+  __shared__ uint32_t tab_all[TAB ? kWavesPerBlock * kWave * kTabStride : 1];
+  uint32_t* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabStride : 0);
 
-  uint32_t step[EPL], kk[EPL];
+  uint32_t step[EPL], kk[EPL], jj[EPL];
   bool act[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) {
     const uint32_t c = c0 + lane + kWave * r;
     act[r] = c < p.d;
     const uint32_t cc = act[r] ? c : 0;
-    const uint32_t j = cc / p.Z;
-    kk[r] = cc - j * p.Z;
-    step[r] = chunk_step(p.a, j);
+    jj[r] = cc / p.Z;
+    kk[r] = cc - jj[r] * p.Z;
+    step[r] = TAB ? 0u : chunk_step(p.a, jj[r]);
   }
   uint32_t key = 0xffffffffu, row = 0;
   if (lane < cnt) {
@@ -259,20 +261,26 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
       }
     }
   }
+  // lane l: chunk bases of the key it holds after the sort
+  if (TAB) fill_base_table(tab, key, p, lane);
   float acc[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
 
   for (int q = 0; q < cnt; q += U) {
+    // Load phase: straight-line, U rows in flight (past-the-end positions
+    // re-read the last row of the piece; inactive dims read the row start).
     float gv[U][EPL];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (q + u < cnt) {
-        const float* grow = grad + static_cast<uint64_t>(readlane_u32(row, q + u)) * p.d + c0 + lane;
+      const int uu = q + u < cnt ? q + u : cnt - 1;
+      const float* grow = grad + static_cast<uint64_t>(readlane_u32(row, uu)) * p.d;
 #pragma unroll
-        for (int r = 0; r < EPL; ++r) gv[u][r] = act[r] ? __builtin_nontemporal_load(grow + kWave * r) : 0.f;
-      }
+      for (int r = 0; r < EPL; ++r)
+        gv[u][r] = __builtin_nontemporal_load(grow + (act[r] ? c0 + lane + kWave * r : 0u));
     }
+    // Reduce phase: deposits (atomics) only after every load of the batch
+    // was issued; loads and atomics share one wait counter on gfx9.
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (q + u < cnt) {
@@ -284,7 +292,8 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
 #pragma unroll
           for (int r = 0; r < EPL; ++r) {
             if (act[r]) {
-              const uint32_t base = fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M);
+              const uint32_t base = TAB ? tab[(q + u) * kTabStride + jj[r]]
+                                        : fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M);
               unsafeAtomicAdd(dst + wrap_add(base, kk[r], p.M), scale * acc[r]);
             }
             acc[r] = 0.f;
@@ -300,15 +309,24 @@ size_t sorted_workspace_bytes(int64_t N) {
   return static_cast<size_t>(N) * 16 + nblocks * kBins * 4 + kBins * 4 + 256;
 }
 
-template <int EPL, int U>
+template <int EPL, int U, bool TAB>
 static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const float* grad, hipStream_t stream) {
   const uint64_t waves = (static_cast<uint64_t>(p.N) + kWave - 1) / kWave;
   const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
-  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U>), dim3(static_cast<uint32_t>(blocks), slabs),
+  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, TAB>), dim3(static_cast<uint32_t>(blocks), slabs),
                      dim3(kBlockThreads), 0, stream, dst, scale, p, keys, rows, grad, p.N);
   return hipGetLastError();
+}
+
+template <bool TAB>
+static hipError_t launch_reduce_c(float* dst, float scale, const KParams& p, const uint32_t* keys,
+                                  const uint32_t* rows, const float* grad, hipStream_t stream) {
+  if (p.d <= 64) return launch_reduce_t<1, 16, TAB>(dst, scale, p, keys, rows, grad, stream);
+  if (p.d <= 128) return launch_reduce_t<2, 8, TAB>(dst, scale, p, keys, rows, grad, stream);
+  if (p.d <= 256) return launch_reduce_t<4, 4, TAB>(dst, scale, p, keys, rows, grad, stream);
+  return launch_reduce_t<8, 2, TAB>(dst, scale, p, keys, rows, grad, stream);
 }
 
 hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const int64_t* indices,
@@ -350,10 +368,8 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
     uint32_t* t = k0; k0 = k1; k1 = t;
     t = v0; v0 = v1; v1 = t;
   }
-  if (p.d <= 64) return launch_reduce_t<1, 16>(dst, scale, p, k0, v0, grad, stream);
-  if (p.d <= 128) return launch_reduce_t<2, 8>(dst, scale, p, k0, v0, grad, stream);
-  if (p.d <= 256) return launch_reduce_t<4, 4>(dst, scale, p, k0, v0, grad, stream);
-  return launch_reduce_t<8, 2>(dst, scale, p, k0, v0, grad, stream);
+  if (p.C <= static_cast<uint32_t>(kTabChunks)) return launch_reduce_c<true>(dst, scale, p, k0, v0, grad, stream);
+  return launch_reduce_c<false>(dst, scale, p, k0, v0, grad, stream);
 }
 
 }  // namespace pss

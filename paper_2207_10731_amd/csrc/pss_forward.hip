@@ -22,6 +22,60 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// One-hot tile: item l of the tile is bag l.  The (h0, bag) pairs are sorted
+// across the lanes; every run of equal h0 is one token, gathered once (U runs
+// in flight) and stored to the rows of all its bags.
+template <typename WT, int EPL, int U>
+__device__ __forceinline__ void forward_onehot_tile(
+    const WT* __restrict__ w, const KParams& p, const Tile& tl,
+    const int64_t* __restrict__ indices, float* __restrict__ out, uint32_t* tab, int lane,
+    uint32_t c0, const uint32_t* jj, const uint32_t* kk, const bool* act) {
+  const int nb = tl.nb;
+  uint32_t key = 0xffffffffu;  // empty lanes sort last
+  uint32_t bag = static_cast<uint32_t>(lane);
+  if (lane < nb) {
+    const uint32_t i = static_cast<uint32_t>(__builtin_nontemporal_load(indices + tl.E0 + lane));
+    key = item_hash(i, tl.tC, p.TC, p.a, p.b);
+  }
+  wave_sort_pairs(key, bag, lane);
+  fill_base_table(tab, key, p, lane);
+  const uint32_t prev = __shfl_up(key, 1);
+  uint64_t starts = __ballot(lane < nb && (lane == 0 || prev != key));
+  while (starts) {
+    // next U runs: first positions pos[u], run u covers [pos[u], pos[u+1])
+    int pos[U + 1];
+#pragma unroll
+    for (int u = 0; u <= U; ++u) {
+      if (starts) {
+        pos[u] = __builtin_ctzll(starts);
+        if (u < U) starts &= starts - 1;
+      } else {
+        pos[u] = nb;
+      }
+    }
+    float v[U][EPL];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int pu = pos[u] < nb ? pos[u] : pos[0];
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) {
+        const uint32_t m = act[r] ? wrap_add(tab[pu * kTabStride + jj[r]], kk[r], p.M) : 0u;
+        v[u][r] = load_weight(w, m);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      for (int q = pos[u]; q < pos[u + 1]; ++q) {
+        const int b = static_cast<int>(readlane_u32(bag, q));
+        const uint64_t ro = readlane_u64(tl.row_off, b) + c0 + lane;
+#pragma unroll
+        for (int r = 0; r < EPL; ++r)
+          if (act[r]) __builtin_nontemporal_store(v[u][r], out + ro + kWave * r);
+      }
+    }
+  }
+}
+
 template <typename WT, int EPL, int U, bool TAB>
 __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     const WT* __restrict__ w, const KParams p, const int64_t* __restrict__ indices,
@@ -48,6 +102,17 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
   }
 
   const Tile tl = load_tile(p, offsets, g0, lane);
+
+  if (TAB) {
+    // One-hot tile (every bag exactly one item): gather each distinct token
+    // of the tile once and store its row to every bag that reads it.
+    const int64_t nxt = __shfl_down(tl.start, 1);
+    const int64_t end = lane == tl.nb - 1 ? tl.E1 : nxt;
+    if (__ballot(lane >= tl.nb || end - tl.start == 1) == ~0ull) {
+      forward_onehot_tile<WT, EPL, U>(w, p, tl, indices, out, tab, lane, c0, jj, kk, act);
+      return;
+    }
+  }
 
   float acc[EPL];
 #pragma unroll

@@ -127,6 +127,27 @@ __device__ __forceinline__ void fill_base_table(uint32_t* tab, uint32_t h0, cons
   }
 }
 
+// Bitonic sort of one (key, payload) pair per lane across the 64 lanes of a
+// wavefront, ascending by key (ties keep no particular order).
+__device__ __forceinline__ void wave_sort_pairs(uint32_t& key, uint32_t& val, int lane) {
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint32_t ok = __shfl_xor(key, j);
+      const uint32_t ov = __shfl_xor(val, j);
+      const bool up = (lane & k) == 0;
+      const bool lower = (lane & j) == 0;
+      // the lower lane of an ascending pair keeps the smaller key
+      const bool take = lower == up ? ok < key : ok > key;
+      if (take) {
+        key = ok;
+        val = ov;
+      }
+    }
+  }
+}
+
 // Local bag (0..nb-1) of item e of the tile: the largest l with start[l] <= e.
 // Binary search over the starts held in the lanes (6 cross-lane reads).
 __device__ __forceinline__ int bag_of_item(const Tile& tl, int64_t e) {

@@ -10,7 +10,7 @@
 //             mod p, identical for identical tokens, 31 bits), r = b*T + t
 //             the pooled row its gradient is read from.
 //   sort      LSD radix sort of the (h0, r) pairs on the low 8, 16 or 24
-//             bits of h0 (groups of about 32 pairs), 8-bit digits, stable;
+//             bits of h0 (groups of at most ~8192 pairs), 8-bit digits, stable;
 //             per pass a histogram kernel, a per-digit scan (one workgroup
 //             per digit) and a scatter kernel whose per-wave ranks come from
 //             ballot matching (no atomics on the data path).
@@ -26,10 +26,11 @@ namespace pss {
 
 constexpr int kSortBits = 8;
 constexpr int kBins = 1 << kSortBits;
-constexpr int kSortItemsPerLane = 16;
+constexpr int kSortItemsPerLane = 8;
 constexpr int kSortTile = kBlockThreads * kSortItemsPerLane;  // keys per block
 constexpr int kWaveSortKeys = kWave * kSortItemsPerLane;       // keys per wave
-static_assert(kBins == kBlockThreads, "one digit per thread in the scatter prologue");
+constexpr int kDigitsPerThread = kBins / kBlockThreads;
+static_assert(kBins % kBlockThreads == 0, "whole digits per thread in the scatter prologue");
 
 // ---------------------------------------------------------------------------
 // keygen
@@ -177,14 +178,25 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint64_t eq = match_digit(digit, valid);
     if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
   }
-  // first slot of each digit: exclusive scan of the digit totals (one digit
-  // per thread)
+  // First slot of each digit: exclusive scan of the digit totals; thread t
+  // owns digits [t*kDigitsPerThread, (t+1)*kDigitsPerThread).
+  const int d0 = threadIdx.x * kDigitsPerThread;
+  uint32_t tot[kDigitsPerThread];
+  uint32_t mine = 0;
+#pragma unroll
+  for (int i = 0; i < kDigitsPerThread; ++i) {
+    tot[i] = totals[d0 + i];
+    mine += tot[i];
+  }
   uint32_t unused;
-  const uint32_t digit_base = block_exclusive_scan(totals[threadIdx.x], wsum, &unused);
+  uint32_t digit_base = block_exclusive_scan(mine, wsum, &unused);
   __syncthreads();
   // wave start offsets: global slot of the tile + counts of earlier waves
-  for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
+#pragma unroll
+  for (int i = 0; i < kDigitsPerThread; ++i) {
+    const int d = d0 + i;
     uint32_t run = digit_base + offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
+    digit_base += tot[i];
 #pragma unroll
     for (int ww = 0; ww < kWavesPerBlock; ++ww) {
       const uint32_t c = cur[ww][d];
@@ -245,22 +257,7 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
   // global sort only orders the low bits, so tokens that share them can
   // arrive interleaved; sorted, each token of the piece forms one run.
   // Empty lanes hold key 0xffffffff (> any hash) and stay at the end.
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const uint32_t ok = __shfl_xor(key, j);
-      const uint32_t orow = __shfl_xor(row, j);
-      const bool up = (lane & k) == 0;
-      const bool lower = (lane & j) == 0;
-      // the lower lane of an ascending pair keeps the smaller key
-      const bool take = lower == up ? ok < key : ok > key;
-      if (take) {
-        key = ok;
-        row = orow;
-      }
-    }
-  }
+  wave_sort_pairs(key, row, lane);
   // lane l: chunk bases of the key it holds after the sort
   if (TAB) fill_base_table(tab, key, p, lane);
   float acc[EPL];
@@ -350,12 +347,17 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // Grouping only needs equal keys close together: sort by the low bits of
-  // h0, enough of them that a group of equal low bits holds about 32 pairs
-  // on average; the reduction's in-register sort then separates the tokens
-  // of a group.  Whole 8-bit passes, at most 24 bits, ping-pong buffers.
+  // Grouping only needs equal keys close together: the pairs are sorted by
+  // the low bits of h0 and the reduction's in-register sort of each 64-pair
+  // piece separates tokens that share them.  Frequent tokens already fill
+  // whole pieces after one 8-bit pass; more bits only pay off once a group
+  // of equal low bits holds many pairs, so a pass is added while the
+  // groups would average more than 8192 pairs (measured on the one-hot and
+  // row-hash workloads: 1.7M pairs -> one 8-bit pass, 6.8M -> two).  Wider
+  // digits group better per pass but cost more in the histogram and scatter
+  // than they save.
   int bits = kSortBits;
-  while (bits < 24 && (static_cast<int64_t>(32) << bits) < N) bits += kSortBits;
+  while (bits < 3 * kSortBits && (N >> bits) > 8192) bits += kSortBits;
   for (int shift = 0; shift < bits; shift += kSortBits) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, N,
                        shift, counts, nblocks);

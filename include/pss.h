@@ -74,13 +74,18 @@ enum {
  *   ATOMIC  every (lookup, dim) contribution added with a float atomic, into
  *           `shared` (SGD on float32 storage) or into a float32 gradient
  *           buffer followed by one streaming optimizer pass.
- *   SORTED  Alg. 1 sparse branch: lookups are grouped by token (radix sort on
- *           the item hash), the output-gradient rows of each token are summed
- *           in registers, and each token's sum is added once at its hashed
- *           addresses (float atomics; a token whose lookups span several
- *           wavefronts adds one partial sum per wavefront).
- * Both variants compute the same G; float summation order is not fixed. */
-enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2 };
+ *   SORTED  lookups are grouped by token (radix sort on the item hash), the
+ *           output-gradient rows of each token are summed in registers, and
+ *           each token's sum is added once at its hashed addresses (float
+ *           atomics; a token whose lookups span several wavefronts adds one
+ *           partial sum per wavefront).
+ *   SPARSE  Alg. 1 sparse branch: the unique locations and summed values of
+ *           pss_gradient_sparse, then the optimizer applied at those
+ *           locations only.  No float atomics: bit-identical run to run.
+ *           Requires N * (d/Z) < 2^32.
+ * ATOMIC and SORTED sum in no fixed order; all variants compute the same G up
+ * to float rounding. */
+enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2, PSS_BWD_SPARSE = 3 };
 #define PSS_BWD_MASK 3u
 
 typedef struct {
@@ -124,6 +129,23 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
 int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
                         const pss_hash_params* hash_params, const int64_t* indices,
                         const int64_t* offsets, const float* grad_out, float lr,
+                        hipStream_t stream);
+
+/* Sparse gradient of the shared array (paper Alg. 1, sparse branch:
+ * findUnique over the read locations, scatter_add of the output gradient):
+ *   locations[0 .. U)  the distinct elements m of `shared` that at least one
+ *                      (lookup, dim) reads, ascending (uint32, m < M)
+ *   values[k]          sum of grad_out over every (lookup, dim) reading
+ *                      locations[k], float32, summed in a fixed order
+ *   *num_unique        U (int64, device memory)
+ * The same G as the dense gradient at those locations.  capacity: length of
+ * the caller's locations/values arrays (device); must be at least
+ * min(M, N*d), else PSS_ERR_INVALID_ARG.  Requires N * (d/Z) < 2^32 (else
+ * PSS_ERR_UNSUPPORTED).  Other arguments as for pss_backward_update; nothing
+ * is updated.  Bit-identical from run to run. */
+int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, const float* grad_out,
+                        uint32_t* locations, float* values, int64_t capacity, int64_t* num_unique,
                         hipStream_t stream);
 
 /* Writes h(indices[e], t(e), j) for every item e and chunk j:

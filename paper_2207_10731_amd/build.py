@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpss.so")
 SOURCES = ["pss_api.hip", "pss_forward.hip", "pss_backward.hip", "pss_sorted.hip",
-           "pss_bench.hip"]
+           "pss_sparse.hip", "pss_bench.hip"]
 ARCH = "gfx950"
 
 CXXFLAGS = [

@@ -62,6 +62,13 @@ KParams make_params(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) 
 std::mutex g_pool_mu;
 std::map<int, hipMemPool_t> g_pools;
 
+// Upper bound on the unique locations of a batch: every lookup reads d
+// elements, and there are M elements.
+int64_t sparse_capacity(int64_t M, const KParams& p) {
+  const int64_t nd = p.N * static_cast<int64_t>(p.d);
+  return nd < M ? nd : M;
+}
+
 hipError_t pool_for_current_device(hipMemPool_t* out) {
   int dev = 0;
   hipError_t st = hipGetDevice(&dev);
@@ -144,12 +151,35 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (state != nullptr && !(hash_params->eps >= 0.f && isfinite(hash_params->eps)))
     return PSS_ERR_INVALID_ARG;
   const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
-  if (variant == 3) return PSS_ERR_INVALID_ARG;
-  const bool sorted = variant != PSS_BWD_ATOMIC;  // AUTO and SORTED
-
   const KParams p = make_params(M, Z, d, hash_params);
   const bool bf16 = hash_params->weight_dtype == PSS_BF16;
+  if (variant == PSS_BWD_SPARSE && p.N * static_cast<int64_t>(p.C) >= (1ll << 32))
+    return PSS_ERR_UNSUPPORTED;
   if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
+
+  if (variant == PSS_BWD_SPARSE) {
+    // Alg. 1 sparse branch: unique locations + summed values, then the
+    // optimizer at those locations only.
+    const int64_t cap = sparse_capacity(M, p);
+    const size_t list_bytes = (static_cast<size_t>(cap) * 8 + 255) & ~size_t(255);
+    const size_t ws_bytes = pss::sparse_workspace_bytes(p);
+    void* ws = nullptr;
+    st = scratch_alloc(&ws, list_bytes + 256 + ws_bytes, stream);
+    if (st != PSS_OK) return st;
+    uint32_t* loc = static_cast<uint32_t*>(ws);
+    float* val = reinterpret_cast<float*>(loc + cap);
+    uint32_t* count = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + list_bytes);
+    void* sws = static_cast<char*>(ws) + list_bytes + 256;
+    hipError_t e = pss::launch_gradient_sparse(p, indices, offsets, grad_out, sws, loc, val, cap,
+                                               count, stream);
+    if (e == hipSuccess)
+      e = pss::launch_sparse_optimizer(shared, bf16, state, loc, val, count, cap, lr,
+                                       hash_params->eps, stream);
+    const hipError_t ef = hipFreeAsync(ws, stream);
+    return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
+  }
+
+  const bool sorted = variant != PSS_BWD_ATOMIC;  // AUTO and SORTED
 
   // SGD on float32 storage is linear in G: deposit -lr * grad directly into
   // the shared array.  Otherwise deposit G into a scratch buffer first.
@@ -175,6 +205,35 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   const hipError_t ef = ws ? hipFreeAsync(ws, stream) : hipSuccess;
   if (e != hipSuccess || ef != hipSuccess) return PSS_ERR_HIP;
   return PSS_OK;
+}
+
+int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, const float* grad_out,
+                        uint32_t* locations, float* values, int64_t capacity, int64_t* num_unique,
+                        hipStream_t stream) {
+  int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  if (offsets == nullptr || grad_out == nullptr || num_unique == nullptr) return PSS_ERR_INVALID_ARG;
+  if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  if (p.N * static_cast<int64_t>(p.C) >= (1ll << 32)) return PSS_ERR_UNSUPPORTED;
+  if (capacity < sparse_capacity(M, p)) return PSS_ERR_INVALID_ARG;
+  if (p.N > 0 && (locations == nullptr || values == nullptr)) return PSS_ERR_INVALID_ARG;
+  void* ws = nullptr;
+  const size_t ws_bytes = 256 + (p.N > 0 ? pss::sparse_workspace_bytes(p) : 0);
+  st = scratch_alloc(&ws, ws_bytes, stream);
+  if (st != PSS_OK) return st;
+  uint32_t* count = static_cast<uint32_t*>(ws);
+  hipError_t e = hipSuccess;
+  if (p.N == 0) {
+    e = pss::launch_zero(reinterpret_cast<float*>(count), 1, stream);
+  } else {
+    e = pss::launch_gradient_sparse(p, indices, offsets, grad_out, static_cast<char*>(ws) + 256,
+                                    locations, values, capacity, count, stream);
+  }
+  if (e == hipSuccess) e = pss::launch_store_count(count, num_unique, stream);
+  const hipError_t ef = hipFreeAsync(ws, stream);
+  return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
 }
 
 int pss_debug_addresses(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,

@@ -148,6 +148,29 @@ __device__ __forceinline__ void wave_sort_pairs(uint32_t& key, uint32_t& val, in
   }
 }
 
+// Exclusive scan over the 256 threads of a block (wave scans + LDS carry).
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum,
+                                                         uint32_t* total) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == kWave - 1) wsum[w] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int ww = 0; ww < kWavesPerBlock; ++ww) {
+    before += ww < w ? wsum[ww] : 0u;
+    all += wsum[ww];
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
 // Local bag (0..nb-1) of item e of the tile: the largest l with start[l] <= e.
 // Binary search over the starts held in the lanes (6 cross-lane reads).
 __device__ __forceinline__ int bag_of_item(const Tile& tl, int64_t e) {

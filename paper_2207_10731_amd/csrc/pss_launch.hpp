@@ -24,6 +24,34 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
                                  const int64_t* offsets, const float* grad, void* workspace,
                                  hipStream_t stream);
 
+// Building blocks of the sorted path, shared with the sparse-gradient path.
+// keygen: keys[e] = item part of the hash of lookup e, rows[e] = b*T + t.
+hipError_t launch_keygen(const KParams& p, const int64_t* indices, const int64_t* offsets,
+                         uint32_t* keys, uint32_t* rows, hipStream_t stream);
+// Stable LSD radix sort of (keys, vals) by the low `bits` bits (8-bit
+// digits); on return keys/vals point at whichever buffer pair holds the
+// result.  scratch: radix_scratch_bytes(n) bytes.
+size_t radix_scratch_bytes(int64_t n);
+hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
+                            int64_t n, int bits, uint32_t* scratch, hipStream_t stream);
+// Bits of the item hash the grouping sort orders for N lookups.
+int grouping_bits(int64_t N);
+
+// Sparse gradient (Alg. 1 sparse branch): ascending unique locations and
+// summed values into locations/values (at most `capacity` entries written),
+// their count into *num_unique32 (device).  workspace:
+// sparse_workspace_bytes(p) bytes.  Requires p.N * p.C < 2^32.
+size_t sparse_workspace_bytes(const KParams& p);
+hipError_t launch_gradient_sparse(const KParams& p, const int64_t* indices, const int64_t* offsets,
+                                  const float* grad, void* workspace, uint32_t* locations,
+                                  float* values, int64_t capacity, uint32_t* num_unique32,
+                                  hipStream_t stream);
+hipError_t launch_store_count(const uint32_t* total, int64_t* out, hipStream_t stream);
+// SGD / Adagrad applied at the listed unique locations only.
+hipError_t launch_sparse_optimizer(void* w, bool bf16, float* state, const uint32_t* loc,
+                                   const float* val, const uint32_t* count, int64_t capacity,
+                                   float lr, float eps, hipStream_t stream);
+
 // Dense optimizer pass over the M elements of a gradient buffer G (G[m] == 0
 // leaves element m untouched).  state == nullptr selects SGD.
 hipError_t launch_optimizer(void* w, bool bf16, float* state, const float* G, int64_t M, float lr,

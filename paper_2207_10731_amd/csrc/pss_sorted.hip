@@ -109,29 +109,6 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
   }
 }
 
-// Exclusive scan over the 256 threads of a block (wave scans + LDS carry).
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum,
-                                                         uint32_t* total) {
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
-  uint32_t x = v;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == kWave - 1) wsum[w] = x;
-  __syncthreads();
-  uint32_t before = 0, all = 0;
-#pragma unroll
-  for (int ww = 0; ww < kWavesPerBlock; ++ww) {
-    before += ww < w ? wsum[ww] : 0u;
-    all += wsum[ww];
-  }
-  __syncthreads();
-  *total = all;
-  return before + x - v;
-}
-
 // Row d of counts (one digit, nblocks entries): exclusive scan in place;
 // totals[d] = the row's sum.  One workgroup per digit.
 __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __restrict__ counts,
@@ -301,9 +278,57 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
   }
 }
 
+size_t radix_scratch_bytes(int64_t n) {
+  const uint64_t nblocks = (static_cast<uint64_t>(n) + kSortTile - 1) / kSortTile;
+  return (nblocks * kBins + kBins) * 4 + 256;
+}
+
 size_t sorted_workspace_bytes(int64_t N) {
-  const uint64_t nblocks = (static_cast<uint64_t>(N) + kSortTile - 1) / kSortTile;
-  return static_cast<size_t>(N) * 16 + nblocks * kBins * 4 + kBins * 4 + 256;
+  return static_cast<size_t>(N) * 16 + radix_scratch_bytes(N);
+}
+
+hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
+                            int64_t n, int bits, uint32_t* scratch, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  const uint32_t nblocks = static_cast<uint32_t>((n + kSortTile - 1) / kSortTile);
+  uint32_t* counts = scratch;
+  uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
+  for (int shift = 0; shift < bits; shift += kSortBits) {
+    hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys, n,
+                       shift, counts, nblocks);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
+                       nblocks, totals);
+    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys,
+                       vals, ktmp, vtmp, n, shift, counts, nblocks, totals);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    uint32_t* t = keys; keys = ktmp; ktmp = t;
+    t = vals; vals = vtmp; vtmp = t;
+  }
+  return hipSuccess;
+}
+
+// Grouping only needs equal keys close together: the pairs are sorted by the
+// low bits of h0 and the in-register sort of each 64-pair piece separates
+// tokens that share them.  Frequent tokens already fill whole pieces after
+// one 8-bit pass; more bits only pay off once a group of equal low bits
+// holds many pairs, so a pass is added while the groups would average more
+// than 8192 pairs (measured on the one-hot and row-hash workloads: 1.7M
+// pairs -> one 8-bit pass, 6.8M -> two).  Wider digits group better per
+// pass but cost more in the histogram and scatter than they save.
+int grouping_bits(int64_t N) {
+  int bits = kSortBits;
+  while (bits < 3 * kSortBits && (N >> bits) > 8192) bits += kSortBits;
+  return bits;
+}
+
+hipError_t launch_keygen(const KParams& p, const int64_t* indices, const int64_t* offsets,
+                         uint32_t* keys, uint32_t* rows, hipStream_t stream) {
+  const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
+  const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  hipLaunchKernelGGL(keygen_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kBlockThreads), 0,
+                     stream, p, indices, offsets, keys, rows);
+  return hipGetLastError();
 }
 
 template <int EPL, int U, bool TAB>
@@ -335,41 +360,10 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   uint32_t* v0 = k0 + N;
   uint32_t* k1 = v0 + N;
   uint32_t* v1 = k1 + N;
-  uint32_t* counts = v1 + N;
-  uint32_t* totals = counts + static_cast<uint64_t>((N + kSortTile - 1) / kSortTile) * kBins;
-  const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
-
-  {
-    const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
-    const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL(keygen_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kBlockThreads), 0,
-                       stream, p, indices, offsets, k0, v0);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  // Grouping only needs equal keys close together: the pairs are sorted by
-  // the low bits of h0 and the reduction's in-register sort of each 64-pair
-  // piece separates tokens that share them.  Frequent tokens already fill
-  // whole pieces after one 8-bit pass; more bits only pay off once a group
-  // of equal low bits holds many pairs, so a pass is added while the
-  // groups would average more than 8192 pairs (measured on the one-hot and
-  // row-hash workloads: 1.7M pairs -> one 8-bit pass, 6.8M -> two).  Wider
-  // digits group better per pass but cost more in the histogram and scatter
-  // than they save.
-  int bits = kSortBits;
-  while (bits < 3 * kSortBits && (N >> bits) > 8192) bits += kSortBits;
-  for (int shift = 0; shift < bits; shift += kSortBits) {
-    hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, N,
-                       shift, counts, nblocks);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
-                       nblocks, totals);
-    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, k0, v0,
-                       k1, v1, N, shift, counts, nblocks, totals);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    uint32_t* t = k0; k0 = k1; k1 = t;
-    t = v0; v0 = v1; v1 = t;
-  }
+  uint32_t* scratch = v1 + N;
+  hipError_t e = launch_keygen(p, indices, offsets, k0, v0, stream);
+  if (e == hipSuccess) e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), scratch, stream);
+  if (e != hipSuccess) return e;
   if (p.C <= static_cast<uint32_t>(kTabChunks)) return launch_reduce_c<true>(dst, scale, p, k0, v0, grad, stream);
   return launch_reduce_c<false>(dst, scale, p, k0, v0, grad, stream);
 }

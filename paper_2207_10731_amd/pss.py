@@ -21,7 +21,7 @@ HEADER = os.path.join(INCLUDE, "pss.h")
 PSS_PRIME = 2**31 - 1
 PSS_F32, PSS_BF16 = 0, 1
 PSS_OK, PSS_ERR_INVALID_ARG, PSS_ERR_UNSUPPORTED, PSS_ERR_HIP, PSS_ERR_NO_MEMORY = 0, 1, 2, 3, 4
-PSS_BWD_AUTO, PSS_BWD_ATOMIC, PSS_BWD_SORTED = 0, 1, 2
+PSS_BWD_AUTO, PSS_BWD_ATOMIC, PSS_BWD_SORTED, PSS_BWD_SPARSE = 0, 1, 2, 3
 
 
 class PssError(RuntimeError):
@@ -60,12 +60,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_forward.argtypes = [vp, i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_backward_update.argtypes = [vp, vp, i64, i32, i32, hp, vp, vp, vp, ctypes.c_float, vp]
     lib.pss_debug_addresses.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
+    lib.pss_gradient_sparse.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp, vp, i64, vp, vp]
     lib.pss_hash_bases_host.argtypes = [i64, i32, i32, hp, vp, vp, vp]
     lib.pss_validate_offsets_host.argtypes = [vp, i64, i64]
     lib.pss_status_string.argtypes = [ctypes.c_int]
     lib.pss_status_string.restype = ctypes.c_char_p
     for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
-                 "pss_debug_addresses", "pss_hash_bases_host", "pss_validate_offsets_host"):
+                 "pss_debug_addresses", "pss_gradient_sparse", "pss_hash_bases_host",
+                 "pss_validate_offsets_host"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -160,6 +162,25 @@ def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, g
     _check(lib.pss_backward_update(_ptr(shared), _ptr(state), M, Z, d, ctypes.byref(hash_params),
                                    _ptr(indices), _ptr(offsets), _ptr(grad_out),
                                    ctypes.c_float(lr), _stream(stream)), "pss_backward_update")
+
+
+def pss_gradient_sparse(M, Z, d, hash_params, indices, offsets, grad_out, locations, values,
+                        num_unique, stream=None):
+    """locations: int32 tensor (uint32 bit patterns), values: float32, both of
+    length >= min(M, N*d); num_unique: int64 tensor of one element."""
+    lib = load_library()
+    _need(indices, torch.int64, "indices")
+    _need(offsets, torch.int64, "offsets")
+    _need(grad_out, torch.float32, "grad_out")
+    _need(locations, torch.int32, "locations")
+    _need(values, torch.float32, "values")
+    _need(num_unique, torch.int64, "num_unique")
+    if locations.numel() != values.numel():
+        raise ValueError("locations and values must have the same length")
+    _check(lib.pss_gradient_sparse(M, Z, d, ctypes.byref(hash_params), _ptr(indices), _ptr(offsets),
+                                   _ptr(grad_out), _ptr(locations), _ptr(values),
+                                   locations.numel(), _ptr(num_unique), _stream(stream)),
+           "pss_gradient_sparse")
 
 
 def pss_debug_addresses(M, Z, d, hash_params, indices, offsets, base_out, stream=None):

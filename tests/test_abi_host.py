@@ -125,9 +125,23 @@ def test_backward_rejects_bad_arguments(lib):
     hp_neg = pss.pss_hash_params(5, 7, 4, 2, 8, 0, -1.0, 0)
     assert f(dummy, dummy, 4096, 4, 16, ctypes.byref(hp_neg), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
-    hp3 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 3)
-    assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp3), dummy, dummy, dummy,
+    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 4)
+    assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp4), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
+
+
+def test_gradient_sparse_rejects_bad_arguments(lib):
+    dummy = ctypes.c_void_p(0x1000)
+    f = lib.pss_gradient_sparse
+    hp = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 0)
+    # capacity below min(M, N*d) = min(4096, 128)
+    assert f(4096, 4, 16, ctypes.byref(hp), dummy, dummy, dummy, dummy, dummy, 127, dummy,
+             None) == pss.PSS_ERR_INVALID_ARG
+    assert f(4096, 4, 16, ctypes.byref(hp), dummy, dummy, dummy, dummy, dummy, 128, None,
+             None) == pss.PSS_ERR_INVALID_ARG
+    big = pss.pss_hash_params(5, 7, 4, 2, 2**31, 0, 1e-10, 0)  # N*C = 2^33
+    assert f(4096, 4, 16, ctypes.byref(big), dummy, dummy, dummy, dummy, dummy, 4096, dummy,
+             None) == pss.PSS_ERR_UNSUPPORTED
 
 
 def test_offsets_validator():

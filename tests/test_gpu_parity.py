@@ -21,7 +21,8 @@ CASES = [("c1", None, None), ("c2", 700, None), ("c3", 50, None), ("c4", 300, 50
          ("c5", 900, None)]
 
 
-VARIANTS = {"atomic": pss.PSS_BWD_ATOMIC, "sorted": pss.PSS_BWD_SORTED}
+VARIANTS = {"atomic": pss.PSS_BWD_ATOMIC, "sorted": pss.PSS_BWD_SORTED,
+            "sparse": pss.PSS_BWD_SPARSE}
 
 
 def _id(c):

@@ -1,0 +1,83 @@
+"""GPU parity of the sparse gradient export (Alg. 1, sparse branch).
+
+Unique locations must equal the oracle's bit for bit (they are integers);
+values must match the oracle's float64 sums within the normalised tolerance;
+two runs must give identical bits (no atomics on this path).
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import pss_oracle as o
+from paper_2207_10731_amd import pss
+from parity import Layer
+
+pytestmark = pytest.mark.gpu
+
+CASES = [("c1", None, {}), ("c2", 700, {}), ("c3", 50, {}), ("c4", 300, dict(M=50_000_000)),
+         ("c5", 900, {}),
+         ("wrap-z3-m61", 33, dict(d=24, Z=3, M=61)), ("z-equals-m", 40, dict(d=32, Z=32, M=32)),
+         ("m-one", 40, dict(d=4, Z=1, M=1)), ("empty-and-long", 70, dict(bag="poisson:30:0:200")),
+         ("d640", 20, dict(d=640, Z=64))]
+
+
+def _wl(key, over):
+    base = synth.get(key if key in synth.CONFIGS else "c1")
+    return base.scaled(**over) if over else base
+
+
+def _run_sparse(L, grad):
+    wl = L.wl
+    dev = L.dev
+    cap = min(wl.M, L.x.N * wl.d) if L.x.N else 1
+    loc = torch.empty(cap, dtype=torch.int32, device=dev)
+    val = torch.empty(cap, dtype=torch.float32, device=dev)
+    nu = torch.empty(1, dtype=torch.int64, device=dev)
+    g = torch.from_numpy(grad).to(dev)
+    pss.pss_gradient_sparse(wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, g, loc, val, nu)
+    torch.cuda.synchronize()
+    n = int(nu.item())
+    return loc[:n].cpu().numpy().view(np.uint32), val[:n].cpu().numpy()
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_sparse_gradient_matches_oracle(case):
+    key, B, over = case
+    L = Layer(_wl(key, over), B=B)
+    wl = L.wl
+    g = synth.make_grad(wl, B=L.B)
+    loc, val = _run_sparse(L, g)
+    uloc, uval = o.gradient_sparse(wl.M, wl.Z, wl.d, wl.T, L.B, L.a, L.b, L.x.indices,
+                                   L.x.offsets, g)
+    assert np.array_equal(loc.astype(np.int64), uloc)
+    _, A, _ = o.gradient_dense(wl.M, wl.Z, wl.d, wl.T, L.B, L.a, L.b, L.x.indices, L.x.offsets, g)
+    err = np.abs(val.astype(np.float64) - uval)
+    assert np.all(err <= 1e-5 * A[uloc] + 1e-30)
+
+
+@pytest.mark.parametrize("key", ["c2", "c3"])
+def test_sparse_gradient_is_deterministic(key):
+    L = Layer(synth.get(key), B=300)
+    g = synth.make_grad(L.wl, B=L.B)
+    loc1, val1 = _run_sparse(L, g)
+    loc2, val2 = _run_sparse(L, g)
+    assert np.array_equal(loc1, loc2)
+    assert np.array_equal(val1.view(np.uint32), val2.view(np.uint32))
+
+
+def test_sparse_gradient_no_lookups():
+    wl = synth.get("c1").scaled(bag="poisson:0:0:0")
+    L = Layer(wl, B=65)
+    loc, val = _run_sparse(L, synth.make_grad(wl, B=65))
+    assert loc.size == 0 and val.size == 0
+
+
+def test_sparse_update_is_deterministic():
+    wl = synth.get("c3")
+    outs = []
+    for _ in range(2):
+        L = Layer(wl, B=200, flags=pss.PSS_BWD_SPARSE, s0=0.1)
+        L.backward(synth.make_grad(wl, B=200))
+        outs.append((L.weights().view(np.uint32).copy(), L.state.cpu().numpy().view(np.uint32)))
+    assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])

@@ -1,0 +1,113 @@
+"""Shape sweeps of the PSS layer on one GPU (the paper's micro-benchmark setup).
+
+The paper times a single embedding table looked up with batch 10240 and
+d = 128, with the loss taken as the sum of all retrieved elements (so the
+output gradient is all ones), while varying the chunk size Z and the
+compression (original table size n*d over |M|); it reports that larger
+chunks help, and that dense gradients win at high compression while sparse
+gradients cost the same at every compression (Sec. 3, appendix
+observations).  This module measures the same sweeps here:
+
+  python -m paper_2207_10731_amd.sweep chunk      forward/backward vs Z
+  python -m paper_2207_10731_amd.sweep crossover  dense vs sparse backward vs |M|
+
+Inputs: n = 10^7 rows, one uniform index per sample, grad_out = 1.
+Each point: median of `--reps` timed calls (HIP events on the stream the
+library launches on) after warm-up.  Output: one markdown table on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import sys
+
+import numpy as np
+import torch
+
+from . import pss
+
+ROWS = 10_000_000
+BATCH = 10240
+DIM = 128
+
+
+def _time(fn, reps, warmup=3):
+    for _ in range(warmup):
+        fn()
+    ts = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e3)
+    return float(np.median(ts))
+
+
+class Point:
+    def __init__(self, M, Z, seed=7, optimizer="sgd", dev="cuda"):
+        rng = np.random.default_rng(seed)
+        self.M, self.Z = int(M), int(Z)
+        self.idx = torch.from_numpy(rng.integers(0, ROWS, BATCH, dtype=np.int64)).to(dev)
+        self.off = torch.arange(BATCH + 1, dtype=torch.int64, device=dev)
+        self.w = torch.from_numpy(rng.uniform(-0.01, 0.01, self.M).astype(np.float32)).to(dev)
+        self.state = torch.zeros(self.M, device=dev) if optimizer == "adagrad" else None
+        self.grad = torch.ones((BATCH, DIM), device=dev)
+        self.out = torch.empty((BATCH, DIM), device=dev)
+        self.seed = seed
+
+    def hp(self, flags):
+        return pss.make_hash_params(self.seed, num_tables=1, batch=BATCH, num_indices=BATCH,
+                                    flags=flags)
+
+    def forward(self):
+        pss.pss_forward(self.w, self.M, self.Z, DIM, self.hp(pss.PSS_BWD_AUTO), self.idx, self.off,
+                        self.out)
+
+    def backward(self, flags, lr=1e-4):
+        pss.pss_backward_update(self.w, self.state, self.M, self.Z, DIM, self.hp(flags), self.idx,
+                                self.off, self.grad, lr)
+
+
+def chunk_sweep(reps):
+    print("| Z | compression | M | forward us | backward (sorted) us | backward (sparse) us |")
+    print("|---|---|---|---|---|---|")
+    for comp in (1000, 10000):
+        M = ROWS * DIM // comp
+        for Z in (1, 2, 4, 8, 16, 32, 64, 128):
+            pt = Point(M, Z)
+            f = _time(pt.forward, reps)
+            b = _time(lambda: pt.backward(pss.PSS_BWD_SORTED), reps)
+            s = _time(lambda: pt.backward(pss.PSS_BWD_SPARSE), reps)
+            print(f"| {Z} | {comp}x | {M} | {f:.1f} | {b:.1f} | {s:.1f} |", flush=True)
+
+
+def crossover_sweep(reps):
+    print("| compression | M | optimizer | dense (sorted) us | dense (atomic) us | sparse us |")
+    print("|---|---|---|---|---|---|")
+    for opt in ("adagrad", "sgd"):
+        for comp in (10, 100, 1000, 10000, 100000):
+            M = ROWS * DIM // comp
+            pt = Point(M, 32, optimizer=opt)
+            d = _time(lambda: pt.backward(pss.PSS_BWD_SORTED), reps)
+            a = _time(lambda: pt.backward(pss.PSS_BWD_ATOMIC), reps)
+            s = _time(lambda: pt.backward(pss.PSS_BWD_SPARSE), reps)
+            print(f"| {comp}x | {M} | {opt} | {d:.1f} | {a:.1f} | {s:.1f} |", flush=True)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("mode", choices=["chunk", "crossover"])
+    ap.add_argument("--reps", type=int, default=20)
+    a = ap.parse_args(argv)
+    assert torch.cuda.is_available(), "the sweep needs a GPU"
+    print(f"<!-- {torch.cuda.get_device_name(0)}; n = {ROWS} rows, batch {BATCH}, d = {DIM}, "
+          f"grad_out = 1, median of {a.reps} -->")
+    (chunk_sweep if a.mode == "chunk" else crossover_sweep)(a.reps)
+
+
+if __name__ == "__main__":
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    main()

@@ -196,3 +196,18 @@ def test_sorted_and_atomic_agree(key):
     bound = 1e-5 * (0.1 + A * A) + 1e-30
     assert np.all(np.abs(sa - ss) <= 2 * bound)
     assert np.all(np.abs(ss - s_ref) <= bound)
+
+
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
+@pytest.mark.parametrize("Z", [1, 32, 128])
+def test_microbenchmark_shape_counts(Z, variant):
+    """The paper's micro-benchmark shape: one table, batch 10240, d = 128,
+    loss = sum of retrieved elements (grad_out = 1).  With w = 0 and lr = 1
+    the update is minus the read count of every element, exactly."""
+    wl = synth.get("c1").scaled(T=1, B=10240, d=128, Z=Z, M=128_000, cardinality="fixed:10000000",
+                                optimizer="sgd", weight_dtype="f32")
+    L = Layer(wl, w=np.zeros(wl.M, dtype=np.float32), flags=VARIANTS[variant])
+    ones = np.ones((L.B, wl.d), dtype=np.float32)
+    L.backward(ones, lr=1.0)
+    _, _, _, _, cnt = L.ref_backward(ones, lr=1.0)
+    assert np.array_equal(L.weights(), -cnt.astype(np.float32))

@@ -96,3 +96,15 @@ def gradient(M, Z, d, T, B, rows_per_table, a, b, indices, offsets, grad_out):
                 G[m] += dV[k]
                 cnt[m] += reads[k]
     return G, cnt
+
+
+def compress(E, M, Z, a, b):
+    """M = S E with the explicit S (Thm. 2), E given as nested lists [T][n][d]."""
+    T, n, d = len(E), len(E[0]), len(E[0][0])
+    keys, S = dense_S(M, Z, d, T, [n] * T, a, b)
+    Mv = [0.0] * M
+    for r, (t, i, c) in enumerate(keys):
+        for m in range(M):
+            if S[r][m]:
+                Mv[m] += float(E[t][i][c])
+    return Mv

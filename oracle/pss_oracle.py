@@ -359,3 +359,43 @@ def backward_update(w, s, M, Z, d, T, B, a, b, indices, offsets, grad_out, lr,
         return sgd_update(w, G, lr, weight_dtype), None, G, A, cnt
     w_new, s_new = adagrad_update(w, s, G, lr, eps, weight_dtype)
     return w_new, s_new, G, A, cnt
+
+
+# ---------------------------------------------------------------------------
+# Post-hoc compression of a given table (Sec. 2.4 with Thm. 2: the flat
+# array is M = S E and token i is retrieved as (S e_i)^T M) and the
+# (1 +- eps) property of Def. 2.
+# ---------------------------------------------------------------------------
+
+
+def table_addresses(M, Z, d, T, n, a, b):
+    """Address of element (t, i, c) of T tables with n rows each: int64 [T, n, d]."""
+    t = np.repeat(np.arange(T, dtype=np.int64), n)
+    i = np.tile(np.arange(n, dtype=np.int64), T)
+    return addresses_from_bases(M, Z, bases_for(M, Z, d, T, a, b, i, t)).reshape(T, n, d)
+
+
+def compress(E, M, Z, a, b):
+    """M = S E for tables E [T, n, d]: element m of the flat array is the sum
+    of the table entries the mapping sends to m.  Returns (Mv, Mabs) in
+    float64, Mabs being the sum of the absolute values of those entries."""
+    E64 = np.asarray(E, dtype=np.float64)
+    T, n, d = E64.shape
+    addr = table_addresses(M, Z, d, T, n, a, b).ravel()
+    Mv = np.bincount(addr, weights=E64.ravel(), minlength=M)
+    Mabs = np.bincount(addr, weights=np.abs(E64).ravel(), minlength=M)
+    return Mv, Mabs
+
+
+def recover(w, M, Z, d, T, n, a, b, weight_dtype=F32):
+    """Retrieved rows (S e_(t,i))^T M of every token of every table: float64 [T, n, d]."""
+    return widen(w, weight_dtype)[table_addresses(M, Z, d, T, n, a, b)]
+
+
+def pss_row_error(E, R):
+    """Per-row eps of Def. 2: sup over x != 0 of |<R_i, x> - <E_i, x>| / ||x||_2.
+
+    By Cauchy-Schwarz the supremum is attained at x = R_i - E_i and equals
+    ||R_i - E_i||_2.  E, R: [..., d]; returns float64 [...]."""
+    D = np.asarray(R, dtype=np.float64) - np.asarray(E, dtype=np.float64)
+    return np.sqrt(np.sum(D * D, axis=-1))

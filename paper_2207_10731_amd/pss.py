@@ -217,3 +217,64 @@ def pss_validate_offsets_host(offsets, num_bags, N) -> int:
 
 def pss_status_string(status: int) -> str:
     return status_string(status)
+
+
+def _table_lookups(T, n, device):
+    """One-item bags over every (t, i) of T tables of n rows, table-major.
+
+    The mapping's key is (i*T + t)*C + j.  Presenting row i of table t as
+    token i*T + t of a single table (T = 1) gives the same key, so bag
+    g = t*n + i reads exactly the chunks of (t, i) and its pooled row
+    [g, 0:d] is element (t, i, :) of a [T, n, d] tensor."""
+    if T * n >= 2**31:
+        raise ValueError("T * n must stay below 2^31")
+    ii = torch.arange(n, dtype=torch.int64, device=device) * T
+    indices = (ii.unsqueeze(0) + torch.arange(T, dtype=torch.int64, device=device).unsqueeze(1))
+    offsets = torch.arange(T * n + 1, dtype=torch.int64, device=device)
+    return indices.reshape(-1), offsets
+
+
+def compress_table(table, M, Z, hash_params, variant=PSS_BWD_SPARSE, out=None, stream=None):
+    """Post-hoc PSS of given tables (Sec. 2.4 with Thm. 2: M = S E).
+
+    table: float32 [T, n, d] on the GPU.  Returns the float32 flat array of
+    M elements whose element m is the sum of every table entry (t, i, c)
+    that the mapping sends to m (``out`` if given, which is overwritten).
+    Only (a, b) of ``hash_params`` are used.  One deposit pass of the
+    library: every row is a one-item bag whose output gradient is the row,
+    applied by SGD with lr = -1 to a zeroed array.  The default SPARSE
+    backward sums each location in a fixed order (bitwise reproducible);
+    PSS_BWD_SORTED / PSS_BWD_ATOMIC are faster and sum in arrival order.
+    """
+    if table.dim() != 3:
+        raise ValueError("table must be [T, n, d]")
+    _need(table, torch.float32, "table")
+    T, n, d = table.shape
+    indices, offsets = _table_lookups(T, n, table.device)
+    hp = pss_hash_params(hash_params.a, hash_params.b, 1, T * n, T * n, PSS_F32,
+                         hash_params.eps, variant)
+    if out is None:
+        out = torch.empty(M, dtype=torch.float32, device=table.device)
+    _need(out, torch.float32, "out")
+    if out.numel() != M:
+        raise ValueError("out must hold M elements")
+    if isinstance(stream, torch.cuda.Stream):
+        with torch.cuda.stream(stream):
+            out.zero_()
+    else:
+        out.zero_()
+    pss_backward_update(out, None, M, Z, d, hp, indices, offsets, table.contiguous().view(T * n, d),
+                        -1.0, stream)
+    return out
+
+
+def lookup_rows(shared, M, Z, d, num_tables, rows, hash_params, stream=None):
+    """Retrieved rows (S e_(t,i))^T M of rows 0 .. rows-1 of every table:
+    float32 [num_tables, rows, d] (one forward pass of one-item bags)."""
+    T = num_tables
+    indices, offsets = _table_lookups(T, rows, shared.device)
+    hp = pss_hash_params(hash_params.a, hash_params.b, 1, T * rows, T * rows,
+                         _weight_dtype(shared), hash_params.eps, PSS_BWD_AUTO)
+    out = torch.empty((T, rows, d), dtype=torch.float32, device=shared.device)
+    pss_forward(shared, M, Z, d, hp, indices, offsets, out.view(T * rows, d), stream)
+    return out

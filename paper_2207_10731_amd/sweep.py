@@ -10,6 +10,10 @@ observations).  This module measures the same sweeps here:
 
   python -m paper_2207_10731_amd.sweep chunk      forward/backward vs Z
   python -m paper_2207_10731_amd.sweep crossover  dense vs sparse backward vs |M|
+  python -m paper_2207_10731_amd.sweep compress   post-hoc M = S E of a given
+                                                  table (Sec. 2.4): time per
+                                                  backward variant and the
+                                                  empirical eps of Def. 2
 
 Inputs: n = 10^7 rows, one uniform index per sample, grad_out = 1.
 Each point: median of `--reps` timed calls (HIP events on the stream the
@@ -97,15 +101,53 @@ def crossover_sweep(reps):
             print(f"| {comp}x | {M} | {opt} | {d:.1f} | {a:.1f} | {s:.1f} |", flush=True)
 
 
+def compress_sweep(reps, Z=32):
+    """One table of ROWS x DIM entries drawn i.i.d. N(0, 1).  For each
+    compression: time of compress_table per backward variant (and the rate
+    at which table entries are read), then the per-row eps of Def. 2,
+    ||(S e_i)^T M - E_i||, against its expectation over the draw of E,
+    sqrt(sum_m load(m)(load(m) - 1) / n) with load from compressing ones."""
+    g = torch.Generator(device="cuda").manual_seed(11)
+    E = torch.randn((1, ROWS, DIM), device="cuda", generator=g)
+    ones = torch.ones_like(E)
+    norm = E[0].norm(dim=1).mean().item()
+    print(f"<!-- Z = {Z}; mean ||E_i|| = {norm:.3f} -->")
+    print("| compression | M | sparse us | sorted us | atomic us | entries/s (best) "
+          "| mean eps | p99 eps | max eps | sqrt E[eps^2] | mean eps / mean norm |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
+    for comp in (10, 100, 1000, 10000):
+        M = ROWS * DIM // comp
+        hp = pss.make_hash_params(21, num_tables=1, batch=ROWS, num_indices=ROWS)
+        out = torch.empty(M, device="cuda")
+        t = {}
+        for name, v in (("sparse", pss.PSS_BWD_SPARSE), ("sorted", pss.PSS_BWD_SORTED),
+                        ("atomic", pss.PSS_BWD_ATOMIC)):
+            t[name] = _time(lambda: pss.compress_table(E, M, Z, hp, variant=v, out=out), reps, 1)
+        pss.compress_table(E, M, Z, hp, out=out)
+        R = pss.lookup_rows(out, M, Z, DIM, 1, ROWS, hp)
+        eps = (R - E).norm(dim=2).flatten()
+        del R
+        load = pss.compress_table(ones, M, Z, hp, variant=pss.PSS_BWD_SORTED)
+        expect = ((load.double() * (load.double() - 1)).sum() / ROWS).sqrt().item()
+        del load
+        e_sorted = eps.sort().values
+        best = min(t.values())
+        print(f"| {comp}x | {M} | {t['sparse']:.0f} | {t['sorted']:.0f} | {t['atomic']:.0f} "
+              f"| {ROWS * DIM / best * 1e6:.3g} | {eps.mean().item():.3f} "
+              f"| {e_sorted[int(0.99 * ROWS)].item():.3f} | {e_sorted[-1].item():.3f} "
+              f"| {expect:.3f} | {eps.mean().item() / norm:.3f} |", flush=True)
+        del eps, e_sorted, out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["chunk", "crossover"])
+    ap.add_argument("mode", choices=["chunk", "crossover", "compress"])
     ap.add_argument("--reps", type=int, default=20)
     a = ap.parse_args(argv)
     assert torch.cuda.is_available(), "the sweep needs a GPU"
     print(f"<!-- {torch.cuda.get_device_name(0)}; n = {ROWS} rows, batch {BATCH}, d = {DIM}, "
           f"grad_out = 1, median of {a.reps} -->")
-    (chunk_sweep if a.mode == "chunk" else crossover_sweep)(a.reps)
+    {"chunk": chunk_sweep, "crossover": crossover_sweep, "compress": compress_sweep}[a.mode](a.reps)
 
 
 if __name__ == "__main__":

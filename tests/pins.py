@@ -18,6 +18,9 @@ Every ``pin_*`` function raises AssertionError when the oracle module ``o``
   pin_sparse_dense       Alg. 1 sparse branch, densified, equals dense branch
   pin_untouched          elements no lookup reads stay bit-identical
   pin_bf16_rounding      nearest-even bfloat16 rounding == torch's
+  pin_compress           post-hoc M = S E and (S e_i)^T M (Sec. 2.4, Thm. 2)
+                         against the explicit S; the injective case; eps of
+                         Def. 2 as a supremum; the distance bound of Thm. 1
 
 The mutation tests plant mistakes in the oracle and require that at least
 one of these pins fails.
@@ -289,6 +292,57 @@ def pin_bf16_rounding(o, seed=9):
     assert (int(nan[0]) & 0x7F80) == 0x7F80 and (int(nan[0]) & 0x7F) != 0
 
 
+def pin_compress(o, seed=10):
+    """M = S E and (S e_i)^T M against the explicit S; the injective case;
+    eps of Def. 2 as the supremum it is defined to be; Thm. 1."""
+    rng = np.random.default_rng(seed)
+    for _ in range(25):
+        T = int(rng.integers(1, 4))
+        n = int(rng.integers(1, 7))
+        d = int(rng.choice([1, 2, 4, 6, 8]))
+        Z = int(rng.choice([z for z in range(1, d + 1) if d % z == 0]))
+        M = int(rng.integers(max(Z, 2), 48))
+        a, b = int(rng.integers(1, P)), int(rng.integers(0, P))
+        E = rng.standard_normal((T, n, d))
+        Mv, Mabs = o.compress(E, M, Z, a, b)
+        want = np.array(brute.compress(E.tolist(), M, Z, a, b))
+        assert np.all(np.abs(Mv - want) <= 1e-12 * (1 + Mabs))
+        w = rng.uniform(-1, 1, M).astype(np.float32)
+        V = brute.virtual_table(w, M, Z, d, T, [n] * T, a, b)
+        R = o.recover(w, M, Z, d, T, n, a, b)
+        for t in range(T):
+            for i in range(n):
+                assert np.array_equal(R[t, i], np.array(V[(t, i)]))
+        # Def. 2: |<R_i - E_i, x>| <= eps_i ||x|| for every x, equality at x = R_i - E_i
+        eps = o.pss_row_error(E, R)
+        for t in range(T):
+            for i in range(n):
+                D = R[t, i] - E[t, i]
+                for x in list(rng.standard_normal((4, d))) + [D]:
+                    nx = np.sqrt((x * x).sum())
+                    if nx > 0:
+                        assert abs(D @ x) <= eps[t, i] * nx * (1 + 1e-12) + 1e-300
+                assert abs(D @ D - eps[t, i] ** 2) <= 1e-12 * (1 + D @ D)
+        # Thm. 1: pairwise distances move by at most eps_i + eps_j
+        R2, E2, e2 = R.reshape(T * n, d), E.reshape(T * n, d), eps.ravel()
+        for p_ in range(T * n):
+            for q in range(T * n):
+                gap = abs(np.linalg.norm(R2[p_] - R2[q]) - np.linalg.norm(E2[p_] - E2[q]))
+                assert gap <= e2[p_] + e2[q] + 1e-12
+    # injective special case: Z = d, a = Z, b = 0, M = n T Z puts the row of
+    # (t, i) at Z (i T + t): compression is a permutation and recovery exact
+    T, n, d = 3, 5, 4
+    E = rng.standard_normal((T, n, d)).astype(np.float32)
+    M = n * T * d
+    Mv, _ = o.compress(E, M, d, d, 0)
+    for t in range(T):
+        for i in range(n):
+            assert np.array_equal(Mv[d * (i * T + t): d * (i * T + t) + d], E[t, i].astype(np.float64))
+    R = o.recover(Mv.astype(np.float32), M, d, d, T, n, d, 0)
+    assert np.array_equal(R, E.astype(np.float64))
+    assert np.all(o.pss_row_error(E, R) == 0)
+
+
 ALL_PINS = [pin_hash_vectors, pin_forward_brute, pin_gradient_brute, pin_integer_forward,
             pin_embedding_bag, pin_mass, pin_finite_difference, pin_sparse_dense,
-            pin_untouched, pin_bf16_rounding]
+            pin_untouched, pin_bf16_rounding, pin_compress]

@@ -89,6 +89,28 @@ def _gradient_last_write_wins(M, Z, d, T, B, a, b, indices, offsets, grad_out):
     return G, A, np.bincount(addr, minlength=M)
 
 
+def _compress_overwrites(E, M, Z, a, b):
+    E64 = np.asarray(E, dtype=np.float64)
+    T, n, d = E64.shape
+    addr = o.table_addresses(M, Z, d, T, n, a, b).ravel()
+    Mv = np.zeros(M)
+    Mv[addr] = E64.ravel()                                               # collisions overwrite
+    Mabs = np.zeros(M)
+    Mabs[addr] = np.abs(E64).ravel()
+    return Mv, Mabs
+
+
+def _recover_token_major(w, M, Z, d, T, n, a, b, weight_dtype=o.F32):
+    addr = o.table_addresses(M, Z, d, T, n, a, b)
+    # reads the (t, i) address block as if it were laid out [n, T, d]
+    return o.widen(w, weight_dtype)[addr.reshape(n, T, d).transpose(1, 0, 2)]
+
+
+def _row_error_squared(E, R):
+    D = np.asarray(R, dtype=np.float64) - np.asarray(E, dtype=np.float64)
+    return np.sum(D * D, axis=-1)                                        # sqrt dropped
+
+
 MUTANTS = {
     "hash_drops_b": ("bases_for", _bases_drop_b),
     "key_swaps_table_and_token": ("bases_for", _bases_swapped_key),
@@ -100,6 +122,9 @@ MUTANTS = {
     "adagrad_stale_accumulator": ("adagrad_update", _adagrad_old_state),
     "bf16_truncates": ("round_to_bf16_bits", _bf16_truncate),
     "scatter_without_accumulation": ("gradient_dense", _gradient_last_write_wins),
+    "compress_overwrites": ("compress", _compress_overwrites),
+    "recover_token_major": ("recover", _recover_token_major),
+    "row_error_squared": ("pss_row_error", _row_error_squared),
 }
 
 

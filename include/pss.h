@@ -22,11 +22,27 @@
  * ---------------------------------------
  * Bags.  There are T*B bags, table-major: bag g = t*B + b holds the token
  *   indices indices[offsets[g] .. offsets[g+1]) of table t for sample b.
- *   offsets: int64[T*B + 1], offsets[0] = 0, non-decreasing,
- *   offsets[T*B] = N.  indices: int64[N], each in [0, 2^31).  Duplicate
- *   indices in a bag count twice; empty bags pool to zero.
- * Pooled rows.  out / grad_out are float32 [B][T*d], row-major:
- *   element (b, t*d + c) belongs to bag t*B + b, embedding dim c.
+ *   offsets: int64[T*B + 1] (int32 with PSS_INDEX_I32), offsets[0] = 0,
+ *   non-decreasing, offsets[T*B] = N.  indices: int64[N] (int32 with
+ *   PSS_INDEX_I32), each in [0, 2^31).  Duplicate indices in a bag count
+ *   twice; empty bags pool to zero.
+ * Pooled rows.  out / grad_out are float32 [B][T*d] (bfloat16 bit patterns
+ *   with PSS_ROWS_BF16), row-major: element (b, t*d + c) belongs to bag
+ *   t*B + b, embedding dim c.
+ * Options (pss_hash_params.flags, beside the backward variant):
+ *   PSS_SIGN_PM1, PSS_SIGN_SPARSE  chunk signs (paper Sec. 2.5, sparse JL
+ *     with independence relaxation: entries of S in {+1, -1, 0} drawn by a
+ *     universal hash).  A second hash h2 = (sign_a * key + sign_b) mod p of
+ *     the same key gives chunk (i, j) a factor s: PM1: s = -1 if
+ *     h2 >= 2^30, else +1.  SPARSE: s = +1 if h2 < q, -1 if q <= h2 < 2q,
+ *     else 0, with q = floor(p / 6).  The forward reads s * shared[...]; the
+ *     backward deposits s * grad.  A chunk of factor 0 is not read: it adds
+ *     nothing and receives nothing.
+ *   PSS_POOL_MEAN  each bag's pooled row is divided by its number of items
+ *     (torch.nn.EmbeddingBag mode "mean"); the backward deposits grad / |bag|.
+ *   PSS_INDEX_I32  indices and offsets are int32.
+ *   PSS_ROWS_BF16  out is written, and grad_out read, as bfloat16 (out is
+ *     rounded to nearest even from the float32 result).
  * Shared array.  `shared` holds M elements of the storage type named by
  *   pss_hash_params.weight_dtype (float32, or bfloat16 bit patterns).
  *   Arithmetic is float32 throughout; bfloat16 values are widened exactly on
@@ -82,11 +98,20 @@ enum {
  *   SPARSE  Alg. 1 sparse branch: the unique locations and summed values of
  *           pss_gradient_sparse, then the optimizer applied at those
  *           locations only.  No float atomics: bit-identical run to run.
- *           Requires N * (d/Z) < 2^32.
+ *           Requires N * (d/Z) < 2^31.
  * ATOMIC and SORTED sum in no fixed order; all variants compute the same G up
  * to float rounding. */
 enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2, PSS_BWD_SPARSE = 3 };
 #define PSS_BWD_MASK 3u
+
+/* Options, bits 2-6 of pss_hash_params.flags (see "Options" above). */
+#define PSS_SIGN_PM1 (1u << 2)
+#define PSS_SIGN_SPARSE (2u << 2)
+#define PSS_SIGN_MASK (3u << 2)
+#define PSS_POOL_MEAN (1u << 4)
+#define PSS_INDEX_I32 (1u << 5)
+#define PSS_ROWS_BF16 (1u << 6)
+#define PSS_FLAGS_ALL 0x7fu
 
 typedef struct {
   uint32_t a;            /* hash multiplier, 1 <= a <= p - 1 */
@@ -96,39 +121,50 @@ typedef struct {
   int64_t num_indices;   /* N = number of entries of `indices` (= offsets[T*B]) */
   int32_t weight_dtype;  /* pss_dtype of `shared` */
   float eps;             /* Adagrad epsilon (ignored by SGD); >= 0 */
-  uint32_t flags;        /* PSS_BWD_* in bits 0-1, other bits must be 0 */
+  uint32_t flags;        /* PSS_BWD_* in bits 0-1, options in bits 2-6; the
+                            sign field 3 << 2 and higher bits are invalid */
+  uint32_t sign_a;       /* sign hash multiplier, 1 <= sign_a <= p - 1
+                            (read only when a sign option is set) */
+  uint32_t sign_b;       /* sign hash offset, 0 <= sign_b <= p - 1 */
 } pss_hash_params;
 
-/* Fills p->a and p->b from `seed` (other fields untouched): with x1, x2 the
- * first two outputs of SplitMix64 (Steele, Lea & Flood 2014) started from
- * state `seed`, a = 1 + (x1 mod (p - 1)) and b = x2 mod p.  Host only.
- * Returns PSS_ERR_INVALID_ARG if p is NULL. */
+/* Fills p->a, p->b, p->sign_a and p->sign_b from `seed` (other fields
+ * untouched): with x1 .. x4 the first four outputs of SplitMix64 (Steele,
+ * Lea & Flood 2014) started from state `seed`, a = 1 + (x1 mod (p - 1)),
+ * b = x2 mod p, sign_a = 1 + (x3 mod (p - 1)), sign_b = x4 mod p.  Host
+ * only.  Returns PSS_ERR_INVALID_ARG if p is NULL. */
 int pss_hash_params_from_seed(uint64_t seed, pss_hash_params* p);
 
 /* Forward: pooled embeddings (paper Sec. 2.4 forward, Sec. 2.5 mapping).
  *   out[b][t*d + j*Z + k] = sum over e in bag t*B+b of
- *                           shared[(h(indices[e], t, j) + k) mod M]
+ *                           s(e, j) * shared[(h(indices[e], t, j) + k) mod M]
+ *   (s = 1 without a sign option; divided by |bag| with PSS_POOL_MEAN)
  * shared   device, M elements of hash_params->weight_dtype, read only
  * M        1 <= M <= p;  Z: 1 <= Z <= M;  d: 1 <= d <= 4096, Z divides d
- * indices  device int64[N];  offsets: device int64[T*B + 1]
- * out      device float32[B][T*d], fully overwritten; must not alias inputs
+ * indices  device int64[N];  offsets: device int64[T*B + 1] (int32 each with
+ *          PSS_INDEX_I32)
+ * out      device float32[B][T*d] (bfloat16 with PSS_ROWS_BF16), fully
+ *          overwritten; must not alias inputs
  * T*(d/Z) must not exceed 2^32. */
 int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
-                const pss_hash_params* hash_params, const int64_t* indices,
-                const int64_t* offsets, float* out, hipStream_t stream);
+                const pss_hash_params* hash_params, const void* indices,
+                const void* offsets, void* out, hipStream_t stream);
 
 /* Backward + optimizer step, in place (paper Sec. 2.4 backward, Alg. 1).
- *   G[m] = sum of grad_out[b][t*d + j*Z + k] over every (item, j, k) whose
- *          address (h + k) mod M equals m
+ *   G[m] = sum of s(e, j) * grad_out[b][t*d + j*Z + k] (divided by |bag| with
+ *          PSS_POOL_MEAN) over every (item e, j, k) whose address
+ *          (h + k) mod M equals m and whose chunk is read (s != 0)
  *   state == NULL : SGD       shared[m] -= lr * G[m]
  *   state != NULL : Adagrad   state[m] += G[m]^2;
  *                             shared[m] -= lr * G[m] / (sqrt(state[m]) + eps)
  * Every element that no lookup reads keeps its exact bits.  shared: device, M elements, updated in place.
  * state: device float32[M] or NULL, updated in place.  grad_out: device
- * float32[B][T*d], read only.  Other arguments as for pss_forward. */
+ * float32[B][T*d] (bfloat16 with PSS_ROWS_BF16), read only.  Other arguments
+ * as for pss_forward.  The SPARSE variant requires N * (d/Z) < 2^31 (else
+ * PSS_ERR_UNSUPPORTED). */
 int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
-                        const pss_hash_params* hash_params, const int64_t* indices,
-                        const int64_t* offsets, const float* grad_out, float lr,
+                        const pss_hash_params* hash_params, const void* indices,
+                        const void* offsets, const void* grad_out, float lr,
                         hipStream_t stream);
 
 /* Sparse gradient of the shared array (paper Alg. 1, sparse branch:
@@ -140,11 +176,12 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
  *   *num_unique        U (int64, device memory)
  * The same G as the dense gradient at those locations.  capacity: length of
  * the caller's locations/values arrays (device); must be at least
- * min(M, N*d), else PSS_ERR_INVALID_ARG.  Requires N * (d/Z) < 2^32 (else
- * PSS_ERR_UNSUPPORTED).  Other arguments as for pss_backward_update; nothing
- * is updated.  Bit-identical from run to run. */
+ * min(M, N*d), else PSS_ERR_INVALID_ARG.  Requires N * (d/Z) < 2^31 (else
+ * PSS_ERR_UNSUPPORTED).  Other arguments and options as for
+ * pss_backward_update (an element read only by chunks of factor 0 is not a
+ * location); nothing is updated.  Bit-identical from run to run. */
 int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
-                        const int64_t* indices, const int64_t* offsets, const float* grad_out,
+                        const void* indices, const void* offsets, const void* grad_out,
                         uint32_t* locations, float* values, int64_t capacity, int64_t* num_unique,
                         hipStream_t stream);
 
@@ -152,15 +189,31 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
  * base_out: device uint32[N][d/Z].  Same arguments and checks as pss_forward;
  * exists so that hashed addresses can be compared bit for bit. */
 int pss_debug_addresses(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
-                        const int64_t* indices, const int64_t* offsets, uint32_t* base_out,
+                        const void* indices, const void* offsets, uint32_t* base_out,
                         hipStream_t stream);
+
+/* Writes the chunk factor s(e, j) (+1, -1 or 0; +1 for every chunk when no
+ * sign option is set) for every item e and chunk j: sign_out: device
+ * int8[N][d/Z].  Same arguments and checks as pss_debug_addresses; the
+ * kernels evaluate the sign hash from the item hash, this export lets it be
+ * compared bit for bit with the definition. */
+int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                    const void* indices, const void* offsets, int8_t* sign_out,
+                    hipStream_t stream);
 
 /* Host evaluation of the same hash code the kernels run (no GPU needed):
  * base_out[e*C + j] = h(indices[e], t(e), j) for host arrays indices[N],
- * offsets[T*B+1] and base_out[N*C].  Returns PSS_ERR_INVALID_ARG on bad
- * arguments or on offsets that are not a valid partition of [0, N). */
+ * offsets[T*B+1] (int64 whatever the flags say) and base_out[N*C].  Returns
+ * PSS_ERR_INVALID_ARG on bad arguments or on offsets that are not a valid
+ * partition of [0, N). */
 int pss_hash_bases_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
                         const int64_t* indices, const int64_t* offsets, uint32_t* base_out);
+
+/* Host evaluation of the chunk factors, through the same route as the
+ * kernels (second hash from the item hash): sign_out[e*C + j] = s(e, j) for
+ * host arrays as in pss_hash_bases_host and sign_out[N*C] (int8). */
+int pss_hash_signs_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, int8_t* sign_out);
 
 /* Host check of a host copy of offsets: offsets[0] == 0, non-decreasing,
  * offsets[T*B] == N.  Returns PSS_OK or PSS_ERR_INVALID_ARG. */

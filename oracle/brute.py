@@ -23,6 +23,18 @@ def base(a, b, M, T, C, t, i, j):
     return ((a * key + b) % P) % M
 
 
+def sign_factor(a2, b2, T, C, t, i, j, mode):
+    """Factor of chunk j of token i of table t from the second hash
+    h2 = (a2 * key + b2) mod p (None mode: always 1)."""
+    if mode is None:
+        return 1
+    h2 = (a2 * ((i * T + t) * C + j) + b2) % P
+    if mode == "pm1":
+        return -1 if h2 >= 2**30 else 1
+    q = P // 6
+    return 1 if h2 < q else (-1 if h2 < 2 * q else 0)
+
+
 def sketch_rows(M, Z, d, T, rows_per_table, a, b):
     """Explicit S as a dict {(t, i, c): column of the single 1}.
 
@@ -38,21 +50,27 @@ def sketch_rows(M, Z, d, T, rows_per_table, a, b):
     return col
 
 
-def dense_S(M, Z, d, T, rows_per_table, a, b):
-    """S as a list of 0/1 rows, row index r(t, i, c) in lexicographic order."""
+def dense_S(M, Z, d, T, rows_per_table, a, b, sign=None):
+    """S as a list of rows, row index r(t, i, c) in lexicographic order.
+
+    Without ``sign`` the single nonzero of a row is 1; with sign = (mode,
+    a2, b2) it is the chunk's factor (+1, -1, or 0: an all-zero row)."""
     col = sketch_rows(M, Z, d, T, rows_per_table, a, b)
+    mode, a2, b2 = sign if sign is not None else (None, 0, 0)
+    C = d // Z
     keys = sorted(col)
     S = []
     for k in keys:
+        t, i, c = k
         row = [0] * M
-        row[col[k]] = 1
+        row[col[k]] = sign_factor(a2, b2, T, C, t, i, c // Z, mode)
         S.append(row)
     return keys, S
 
 
-def virtual_table(w, M, Z, d, T, rows_per_table, a, b):
+def virtual_table(w, M, Z, d, T, rows_per_table, a, b, sign=None):
     """V[(t, i)] = (S e_(t,i))^T w as lists of floats, via the dense S."""
-    keys, S = dense_S(M, Z, d, T, rows_per_table, a, b)
+    keys, S = dense_S(M, Z, d, T, rows_per_table, a, b, sign)
     V = {}
     for r, (t, i, c) in enumerate(keys):
         V.setdefault((t, i), [0.0] * d)
@@ -60,40 +78,49 @@ def virtual_table(w, M, Z, d, T, rows_per_table, a, b):
     return V
 
 
-def forward(w, M, Z, d, T, B, rows_per_table, a, b, indices, offsets):
-    """Pooled embeddings [B][T*d] as Python floats (exact sums of doubles)."""
-    V = virtual_table(w, M, Z, d, T, rows_per_table, a, b)
+def forward(w, M, Z, d, T, B, rows_per_table, a, b, indices, offsets, sign=None, mean=False):
+    """Pooled embeddings [B][T*d] as Python floats (sums of doubles; with
+    ``mean`` each nonempty bag's sum is divided by its length)."""
+    V = virtual_table(w, M, Z, d, T, rows_per_table, a, b, sign)
     out = [[0.0] * (T * d) for _ in range(B)]
     for t in range(T):
         for bb in range(B):
             g = t * B + bb
+            n = int(offsets[g + 1]) - int(offsets[g])
             for e in range(int(offsets[g]), int(offsets[g + 1])):
                 i = int(indices[e])
                 for c in range(d):
                     out[bb][t * d + c] += V[(t, i)][c]
+            if mean and n:
+                for c in range(d):
+                    out[bb][t * d + c] /= n
     return out
 
 
-def gradient(M, Z, d, T, B, rows_per_table, a, b, indices, offsets, grad_out):
+def gradient(M, Z, d, T, B, rows_per_table, a, b, indices, offsets, grad_out, sign=None,
+             mean=False):
     """G = S^T (dL/dV) with dL/dV[(t, i)][c] = sum of grad_out over the bags
-    that contain token i of table t (with multiplicity).  Returns (G, cnt)."""
-    keys, S = dense_S(M, Z, d, T, rows_per_table, a, b)
+    that contain token i of table t (with multiplicity; divided by the bag's
+    length with ``mean``).  Returns (G, cnt), cnt counting the reads of each
+    element (a zero entry of S is no read)."""
+    keys, S = dense_S(M, Z, d, T, rows_per_table, a, b, sign)
     dV = {k: 0.0 for k in keys}
     reads = {k: 0 for k in keys}
     for t in range(T):
         for bb in range(B):
             g = t * B + bb
+            n = int(offsets[g + 1]) - int(offsets[g])
             for e in range(int(offsets[g]), int(offsets[g + 1])):
                 i = int(indices[e])
                 for c in range(d):
-                    dV[(t, i, c)] += float(grad_out[bb][t * d + c])
+                    dV[(t, i, c)] += float(grad_out[bb][t * d + c]) / (n if mean else 1)
                     reads[(t, i, c)] += 1
     G = [0.0] * M
     cnt = [0] * M
     for r, k in enumerate(keys):
         for m in range(M):
             if S[r][m]:
-                G[m] += dV[k]
+                G[m] += S[r][m] * dV[k]
                 cnt[m] += reads[k]
     return G, cnt
 

@@ -66,6 +66,12 @@ def hash_params_from_seed(seed: int) -> tuple[int, int]:
     return a, b
 
 
+def sign_params_from_seed(seed: int) -> tuple[int, int]:
+    """(a2, b2) of the second (sign) hash: outputs 3 and 4 of the same stream."""
+    x = splitmix64(seed, 4)
+    return 1 + (x[2] % (P - 1)), x[3] % P
+
+
 # ---------------------------------------------------------------------------
 # Validation (same categories as the C ABI; raises ValueError)
 # ---------------------------------------------------------------------------
@@ -149,6 +155,56 @@ def element_addresses(M, Z, d, T, B, a, b, indices, offsets):
 
 
 # ---------------------------------------------------------------------------
+# Optional sign of each chunk (Sec. 2.5, sparse JL with independence
+# relaxation: the entries of S are 0 with probability 2/3 and +1 / -1 with
+# probability 1/6 each, generated on the fly by universal hashing).  Reading
+# used here: a second universal hash of the same key,
+#     h2 = (a2 * key + b2) mod p,
+# decides the factor of the whole chunk (i, j):
+#   "pm1"    : -1 if h2 >= 2^30 else +1            (random signs only)
+#   "sparse" : +1 if h2 < q, -1 if q <= h2 < 2q, else 0,   q = floor(p / 6)
+# A factor of 0 means the chunk is not read at all: it contributes nothing to
+# the forward and receives no gradient.  ``sign`` arguments below are None
+# (no sign, the ROBE-Z mapping as printed) or a tuple (mode, a2, b2).
+# ---------------------------------------------------------------------------
+
+SIGN_PM1 = "pm1"
+SIGN_SPARSE = "sparse"
+Q6 = P // 6  # 357913941
+
+
+def signs_for(Z, d, T, a2, b2, idx, t, mode):
+    """Factor (+1, -1 or 0) of chunk j of items with token ``idx`` in table ``t``: int64 [n, C]."""
+    C = d // Z
+    i = np.asarray(idx, dtype=np.int64).astype(np.uint64)
+    tt = np.asarray(t, dtype=np.int64).astype(np.uint64)
+    j = np.arange(C, dtype=np.uint64)
+    key = (i * np.uint64(T) + tt)[:, None] * np.uint64(C) + j[None, :]
+    h2 = ((np.uint64(a2) * (key % np.uint64(P)) + np.uint64(b2)) % np.uint64(P)).astype(np.int64)
+    if mode == SIGN_PM1:
+        return np.where(h2 >= 2**30, -1, 1).astype(np.int64)
+    if mode == SIGN_SPARSE:
+        return np.where(h2 < Q6, 1, np.where(h2 < 2 * Q6, -1, 0)).astype(np.int64)
+    raise ValueError("unknown sign mode")
+
+
+def element_factors(Z, d, T, B, offsets, indices, sign):
+    """Factor of every read element, float64 [N, d] (chunk factor repeated Z times)."""
+    mode, a2, b2 = sign
+    _, t, _ = item_bags(T, B, offsets)
+    return np.repeat(signs_for(Z, d, T, a2, b2, indices, t, mode), Z, axis=1).astype(np.float64)
+
+
+def item_scale(T, B, offsets, mean):
+    """Per-item weight of its bag's pooled row: 1, or 1/|bag| for mean pooling."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    g, _, _ = item_bags(T, B, offsets)
+    if not mean:
+        return np.ones(g.shape[0])
+    return 1.0 / np.diff(offsets)[g].astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
 # Storage types
 # ---------------------------------------------------------------------------
 
@@ -198,15 +254,24 @@ def round_storage(x64, weight_dtype=F32):
 # ---------------------------------------------------------------------------
 
 
-def forward64(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32):
+def _signed(rows, fac):
+    """fac * rows with a factor of 0 giving exactly 0 (the element is not read)."""
+    return rows if fac is None else np.where(fac == 0, 0.0, fac * rows)
+
+
+def forward64(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32, sign=None,
+              mean=False):
     """Pooled embeddings in float64, [B, T*d], plus sum of |terms| per output.
 
-    out[b, t*d + c] = sum over items e of bag (t, b) of w[addr(e, c)].
-    An empty bag gives 0.
+    out[b, t*d + c] = sum over items e of bag (t, b) of w[addr(e, c)]
+    (times the chunk's factor when ``sign`` is given; divided by |bag| when
+    ``mean``).  An empty bag gives 0.
     """
     offsets = np.asarray(offsets, dtype=np.int64)
     addr = element_addresses(M, Z, d, T, B, a, b, indices, offsets)
     rows = widen(np.asarray(w)[addr], weight_dtype)  # [N, d]
+    if sign is not None:
+        rows = _signed(rows, element_factors(Z, d, T, B, offsets, indices, sign))
     out = np.zeros((T * B, d))
     s_abs = np.zeros((T * B, d))
     lengths = np.diff(offsets)
@@ -215,13 +280,17 @@ def forward64(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32):
         starts = offsets[:-1][nonempty]
         out[nonempty] = np.add.reduceat(rows, starts, axis=0)
         s_abs[nonempty] = np.add.reduceat(np.abs(rows), starts, axis=0)
+        if mean:
+            out[nonempty] /= lengths[nonempty, None]
+            s_abs[nonempty] /= lengths[nonempty, None]
     # bag g = t*B + b  ->  out[b, t*d : (t+1)*d]
     out = out.reshape(T, B, d).transpose(1, 0, 2).reshape(B, T * d)
     s_abs = s_abs.reshape(T, B, d).transpose(1, 0, 2).reshape(B, T * d)
     return out, s_abs
 
 
-def forward_at(w, M, Z, d, T, B, a, b, indices, offsets, bags, weight_dtype=F32):
+def forward_at(w, M, Z, d, T, B, a, b, indices, offsets, bags, weight_dtype=F32, sign=None,
+               mean=False):
     """Pooled float64 rows of the listed bags g = t*B + b only: ([nb, d], s_abs).
 
     Same sums as ``forward64``; used to check sampled bags of large batches.
@@ -239,14 +308,19 @@ def forward_at(w, M, Z, d, T, B, a, b, indices, offsets, bags, weight_dtype=F32)
         t = np.full(hi - lo, g // B, dtype=np.int64)
         addr = addresses_from_bases(M, Z, bases_for(M, Z, d, T, a, b, indices[lo:hi], t))
         rows = widen(w[addr], weight_dtype)
-        out[r] = rows.sum(axis=0)
-        s_abs[r] = np.abs(rows).sum(axis=0)
+        if sign is not None:
+            mode, a2, b2 = sign
+            fac = np.repeat(signs_for(Z, d, T, a2, b2, indices[lo:hi], t, mode), Z, axis=1)
+            rows = _signed(rows, fac.astype(np.float64))
+        div = float(hi - lo) if mean else 1.0
+        out[r] = rows.sum(axis=0) / div
+        s_abs[r] = np.abs(rows).sum(axis=0) / div
     return out, s_abs
 
 
-def forward(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32):
+def forward(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32, sign=None, mean=False):
     """Pooled embeddings rounded once to float32, [B, T*d]."""
-    out64, _ = forward64(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype)
+    out64, _ = forward64(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype, sign, mean)
     return out64.astype(np.float32)
 
 
@@ -255,37 +329,47 @@ def forward(w, M, Z, d, T, B, a, b, indices, offsets, weight_dtype=F32):
 # ---------------------------------------------------------------------------
 
 
-def _contributions(M, Z, d, T, B, a, b, indices, offsets, grad_out):
-    """Flattened (address, upstream gradient) pairs of every read element."""
+def _contributions(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign=None, mean=False):
+    """Flattened (address, upstream gradient) pairs of every read element.
+
+    With mean pooling an item's share of its bag's gradient row is the row
+    divided by |bag|; with a sign the chunk's factor multiplies it and
+    chunks of factor 0 contribute nothing."""
     addr = element_addresses(M, Z, d, T, B, a, b, indices, offsets)
     _, t, bb = item_bags(T, B, offsets)
     g = np.asarray(grad_out, dtype=np.float64).reshape(B, T, d)[bb, t, :]
-    return addr.ravel(), g.ravel()
+    if mean:
+        g = g * item_scale(T, B, offsets, True)[:, None]
+    if sign is None:
+        return addr.ravel(), g.ravel()
+    fac = element_factors(Z, d, T, B, offsets, indices, sign).ravel()
+    keep = fac != 0
+    return addr.ravel()[keep], (g.ravel() * fac)[keep]
 
 
-def gradient_dense(M, Z, d, T, B, a, b, indices, offsets, grad_out):
+def gradient_dense(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign=None, mean=False):
     """Alg. 1, dense branch: G = zeros(M).scatter_add(addresses, grad values).
 
     Returns (G, A, cnt): the float64 gradient, the sum of |contributions| per
     element and the number of contributions per element.
     """
-    addr, g = _contributions(M, Z, d, T, B, a, b, indices, offsets, grad_out)
+    addr, g = _contributions(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign, mean)
     G = np.bincount(addr, weights=g, minlength=M)
     A = np.bincount(addr, weights=np.abs(g), minlength=M)
     cnt = np.bincount(addr, minlength=M)
     return G, A, cnt
 
 
-def gradient_sparse(M, Z, d, T, B, a, b, indices, offsets, grad_out):
+def gradient_sparse(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign=None, mean=False):
     """Alg. 1, sparse branch: unique addresses and the summed values there."""
-    addr, g = _contributions(M, Z, d, T, B, a, b, indices, offsets, grad_out)
+    addr, g = _contributions(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign, mean)
     unique, inverse = np.unique(addr, return_inverse=True)
     vals = np.zeros(unique.shape[0])
     np.add.at(vals, inverse, g)
     return unique, vals
 
 
-def gradient_at(M, Z, d, T, B, a, b, indices, offsets, grad_out, where):
+def gradient_at(M, Z, d, T, B, a, b, indices, offsets, grad_out, where, sign=None, mean=False):
     """G, A and cnt restricted to the flat-array elements listed in ``where``.
 
     Same sums as ``gradient_dense`` without an M-sized result; used to check
@@ -303,6 +387,7 @@ def gradient_at(M, Z, d, T, B, a, b, indices, offsets, grad_out, where):
     indices = np.asarray(indices, dtype=np.int64)
     grad3 = np.asarray(grad_out).reshape(B, T, d)
     gbag, t_all, b_all = item_bags(T, B, offsets)
+    scale = item_scale(T, B, offsets, mean)
     N = indices.shape[0]
     # one flat-array element per output dim: split the items into blocks
     block = max(1, 4_000_000 // max(d, 1))
@@ -316,8 +401,14 @@ def gradient_at(M, Z, d, T, B, a, b, indices, offsets, grad_out, where):
         hit = sw[pos_c] == addr
         if not hit.any():
             continue
+        if sign is not None:
+            mode, a2, b2 = sign
+            fac = np.repeat(signs_for(Z, d, T, a2, b2, idx, tt, mode), Z, axis=1)
+            hit &= fac != 0
         ei, ci = np.nonzero(hit)
-        vals = grad3[b_all[s:e][ei], tt[ei], ci].astype(np.float64)
+        vals = grad3[b_all[s:e][ei], tt[ei], ci].astype(np.float64) * scale[s:e][ei]
+        if sign is not None:
+            vals = vals * fac[ei, ci]
         slot = pos_c[ei, ci]
         np.add.at(G, order[slot], vals)
         np.add.at(A, order[slot], np.abs(vals))
@@ -349,12 +440,12 @@ def adagrad_update(w, s, G, lr, eps, weight_dtype=F32):
 
 
 def backward_update(w, s, M, Z, d, T, B, a, b, indices, offsets, grad_out, lr,
-                    eps=1e-10, weight_dtype=F32):
+                    eps=1e-10, weight_dtype=F32, sign=None, mean=False):
     """Full backward + fused update.  ``s is None`` selects SGD, else Adagrad.
 
     Returns (w_new, s_new or None, G, A, cnt).
     """
-    G, A, cnt = gradient_dense(M, Z, d, T, B, a, b, indices, offsets, grad_out)
+    G, A, cnt = gradient_dense(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign, mean)
     if s is None:
         return sgd_update(w, G, lr, weight_dtype), None, G, A, cnt
     w_new, s_new = adagrad_update(w, s, G, lr, eps, weight_dtype)

@@ -33,7 +33,14 @@ int check_common(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) {
   if (TC >= (1ull << 32)) return PSS_ERR_INVALID_ARG;
   if (hp->num_indices < 0 || hp->num_indices > kMaxItems) return PSS_ERR_INVALID_ARG;
   if (hp->weight_dtype != PSS_F32 && hp->weight_dtype != PSS_BF16) return PSS_ERR_UNSUPPORTED;
-  if (hp->flags & ~PSS_BWD_MASK) return PSS_ERR_INVALID_ARG;
+  if (hp->flags & ~PSS_FLAGS_ALL) return PSS_ERR_INVALID_ARG;
+  if ((hp->flags & PSS_SIGN_MASK) == PSS_SIGN_MASK) return PSS_ERR_INVALID_ARG;
+  if (hp->flags & PSS_SIGN_MASK) {
+    if (hp->sign_a < 1 || hp->sign_a > PSS_PRIME - 1) return PSS_ERR_INVALID_ARG;
+    if (hp->sign_b > PSS_PRIME - 1) return PSS_ERR_INVALID_ARG;
+  }
+  // int32 offsets cannot describe more than 2^31 - 1 items
+  if ((hp->flags & PSS_INDEX_I32) && hp->num_indices > INT32_MAX) return PSS_ERR_INVALID_ARG;
   return PSS_OK;
 }
 
@@ -53,6 +60,19 @@ KParams make_params(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hp) 
   p.d = static_cast<uint32_t>(d);
   p.TC = p.T * p.C;
   p.row_stride = p.T * p.d;
+  p.sign_mode = (hp->flags & PSS_SIGN_MASK) >> 2;
+  p.s_alpha = p.s_beta = p.a2 = 0;
+  if (p.sign_mode) {
+    // h2_0 = a2 * key_0 + b2 = alpha * h_0 + beta (mod p), key_0 = (h_0 - b) / a
+    const uint32_t a_inv = pss::pow_mod_p(p.a, PSS_PRIME - 2);
+    p.a2 = hp->sign_a;
+    p.s_alpha = pss::mod_p(static_cast<uint64_t>(hp->sign_a) * a_inv);
+    const uint32_t ab = pss::mod_p(static_cast<uint64_t>(p.s_alpha) * p.b);
+    p.s_beta = pss::mod_p(static_cast<uint64_t>(hp->sign_b) + PSS_PRIME - ab);
+  }
+  p.mean = (hp->flags & PSS_POOL_MEAN) ? 1u : 0u;
+  p.idx32 = (hp->flags & PSS_INDEX_I32) ? 1u : 0u;
+  p.rows_bf16 = (hp->flags & PSS_ROWS_BF16) ? 1u : 0u;
   return p;
 }
 
@@ -122,14 +142,18 @@ int pss_hash_params_from_seed(uint64_t seed, pss_hash_params* p) {
   uint64_t state = seed;
   const uint64_t x1 = splitmix64_next(&state);
   const uint64_t x2 = splitmix64_next(&state);
+  const uint64_t x3 = splitmix64_next(&state);
+  const uint64_t x4 = splitmix64_next(&state);
   p->a = static_cast<uint32_t>(1 + x1 % (PSS_PRIME - 1));
   p->b = static_cast<uint32_t>(x2 % PSS_PRIME);
+  p->sign_a = static_cast<uint32_t>(1 + x3 % (PSS_PRIME - 1));
+  p->sign_b = static_cast<uint32_t>(x4 % PSS_PRIME);
   return PSS_OK;
 }
 
 int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
-                const pss_hash_params* hash_params, const int64_t* indices,
-                const int64_t* offsets, float* out, hipStream_t stream) {
+                const pss_hash_params* hash_params, const void* indices,
+                const void* offsets, void* out, hipStream_t stream) {
   const int st = check_common(M, Z, d, hash_params);
   if (st != PSS_OK) return st;
   if (shared == nullptr || offsets == nullptr || out == nullptr) return PSS_ERR_INVALID_ARG;
@@ -140,8 +164,8 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
 }
 
 int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
-                        const pss_hash_params* hash_params, const int64_t* indices,
-                        const int64_t* offsets, const float* grad_out, float lr,
+                        const pss_hash_params* hash_params, const void* indices,
+                        const void* offsets, const void* grad_out, float lr,
                         hipStream_t stream) {
   int st = check_common(M, Z, d, hash_params);
   if (st != PSS_OK) return st;
@@ -153,7 +177,7 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
   const KParams p = make_params(M, Z, d, hash_params);
   const bool bf16 = hash_params->weight_dtype == PSS_BF16;
-  if (variant == PSS_BWD_SPARSE && p.N * static_cast<int64_t>(p.C) >= (1ll << 32))
+  if (variant == PSS_BWD_SPARSE && p.N * static_cast<int64_t>(p.C) >= (1ll << 31))
     return PSS_ERR_UNSUPPORTED;
   if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
 
@@ -185,7 +209,7 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   // the shared array.  Otherwise deposit G into a scratch buffer first.
   const bool fused = state == nullptr && !bf16;
   const size_t g_bytes = fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
-  const size_t ws_bytes = sorted ? pss::sorted_workspace_bytes(p.N) : 0;
+  const size_t ws_bytes = sorted ? pss::sorted_workspace_bytes(p) : 0;
   void* ws = nullptr;
   if (g_bytes + ws_bytes > 0) {
     st = scratch_alloc(&ws, g_bytes + ws_bytes, stream);
@@ -208,7 +232,7 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
 }
 
 int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
-                        const int64_t* indices, const int64_t* offsets, const float* grad_out,
+                        const void* indices, const void* offsets, const void* grad_out,
                         uint32_t* locations, float* values, int64_t capacity, int64_t* num_unique,
                         hipStream_t stream) {
   int st = check_common(M, Z, d, hash_params);
@@ -216,7 +240,7 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
   if (offsets == nullptr || grad_out == nullptr || num_unique == nullptr) return PSS_ERR_INVALID_ARG;
   if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
   const KParams p = make_params(M, Z, d, hash_params);
-  if (p.N * static_cast<int64_t>(p.C) >= (1ll << 32)) return PSS_ERR_UNSUPPORTED;
+  if (p.N * static_cast<int64_t>(p.C) >= (1ll << 31)) return PSS_ERR_UNSUPPORTED;
   if (capacity < sparse_capacity(M, p)) return PSS_ERR_INVALID_ARG;
   if (p.N > 0 && (locations == nullptr || values == nullptr)) return PSS_ERR_INVALID_ARG;
   void* ws = nullptr;
@@ -237,7 +261,7 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
 }
 
 int pss_debug_addresses(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
-                        const int64_t* indices, const int64_t* offsets, uint32_t* base_out,
+                        const void* indices, const void* offsets, uint32_t* base_out,
                         hipStream_t stream) {
   const int st = check_common(M, Z, d, hash_params);
   if (st != PSS_OK) return st;
@@ -245,7 +269,19 @@ int pss_debug_addresses(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
   if (hash_params->num_indices > 0 && (indices == nullptr || base_out == nullptr))
     return PSS_ERR_INVALID_ARG;
   const KParams p = make_params(M, Z, d, hash_params);
-  return hip_status(pss::launch_debug_addresses(p, indices, offsets, base_out, stream));
+  return hip_status(pss::launch_debug_addresses(p, indices, offsets, base_out, nullptr, stream));
+}
+
+int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                    const void* indices, const void* offsets, int8_t* sign_out,
+                    hipStream_t stream) {
+  const int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  if (offsets == nullptr) return PSS_ERR_INVALID_ARG;
+  if (hash_params->num_indices > 0 && (indices == nullptr || sign_out == nullptr))
+    return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  return hip_status(pss::launch_debug_addresses(p, indices, offsets, nullptr, sign_out, stream));
 }
 
 int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N) {
@@ -271,6 +307,35 @@ int pss_hash_bases_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
       const uint32_t i = static_cast<uint32_t>(indices[e]);
       for (uint32_t j = 0; j < p.C; ++j)
         base_out[e * p.C + j] = pss::chunk_base(i, t, j, p.C, p.TC, p.a, p.b, p.fm_c, p.M);
+    }
+  }
+  return PSS_OK;
+}
+
+int pss_hash_signs_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                        const int64_t* indices, const int64_t* offsets, int8_t* sign_out) {
+  const int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  const int64_t bags = static_cast<int64_t>(hash_params->num_tables) * hash_params->batch;
+  const int64_t N = hash_params->num_indices;
+  if (pss_validate_offsets_host(offsets, bags, N) != PSS_OK) return PSS_ERR_INVALID_ARG;
+  if (N > 0 && (indices == nullptr || sign_out == nullptr)) return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  for (int64_t g = 0; g < bags; ++g) {
+    const uint32_t t = static_cast<uint32_t>(g / p.B);
+    for (int64_t e = offsets[g]; e < offsets[g + 1]; ++e) {
+      const uint32_t i = static_cast<uint32_t>(indices[e]);
+      const uint32_t h0 = pss::item_hash(i, t * p.C, p.TC, p.a, p.b);
+      const uint32_t h20 = p.sign_mode ? pss::sign_hash0(h0, p.s_alpha, p.s_beta) : 0u;
+      for (uint32_t j = 0; j < p.C; ++j) {
+        int8_t f = 1;
+        if (p.sign_mode) {
+          const uint32_t code =
+              pss::sign_code(pss::add_mod_p(h20, pss::chunk_step(p.a2, j)), p.sign_mode);
+          f = code == 0 ? 1 : (code == 1 ? -1 : 0);
+        }
+        sign_out[e * p.C + j] = f;
+      }
     }
   }
   return PSS_OK;

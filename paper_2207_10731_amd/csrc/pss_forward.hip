@@ -12,6 +12,11 @@
 // On gfx9 stores and loads share one wait counter, so the kernel issues all
 // U gathers of a batch before any store of that batch: a store is never
 // followed by a wait for a load issued after it.
+//
+// Options: SIGN (template) multiplies each chunk by its sign factor and skips
+// chunks of factor 0; mean pooling divides a finished row by the bag's item
+// count; rows may be stored as bfloat16 (round to nearest even); indices and
+// offsets may be int32.
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -22,23 +27,31 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// Pooled value k of the output: float32, or bfloat16 rounded to nearest even.
+__device__ __forceinline__ void store_out(void* out, uint64_t k, float v, uint32_t bf16) {
+  if (bf16)
+    __builtin_nontemporal_store(f32_to_bf16_rne(v), static_cast<uint16_t*>(out) + k);
+  else
+    __builtin_nontemporal_store(v, static_cast<float*>(out) + k);
+}
+
 // One-hot tile: item l of the tile is bag l.  The (h0, bag) pairs are sorted
 // across the lanes; every run of equal h0 is one token, gathered once (U runs
 // in flight) and stored to the rows of all its bags.
-template <typename WT, int EPL, int U>
+template <typename WT, int EPL, int U, bool SIGN>
 __device__ __forceinline__ void forward_onehot_tile(
-    const WT* __restrict__ w, const KParams& p, const Tile& tl,
-    const int64_t* __restrict__ indices, float* __restrict__ out, uint32_t* tab, int lane,
-    uint32_t c0, const uint32_t* jj, const uint32_t* kk, const bool* act) {
+    const WT* __restrict__ w, const KParams& p, const Tile& tl, const void* __restrict__ indices,
+    void* __restrict__ out, uint32_t* tab, int lane, uint32_t c0, const uint32_t* jj,
+    const uint32_t* kk, const bool* act) {
   const int nb = tl.nb;
   uint32_t key = 0xffffffffu;  // empty lanes sort last
   uint32_t bag = static_cast<uint32_t>(lane);
   if (lane < nb) {
-    const uint32_t i = static_cast<uint32_t>(__builtin_nontemporal_load(indices + tl.E0 + lane));
+    const uint32_t i = load_index(indices, tl.E0 + lane, p.idx32);
     key = item_hash(i, tl.tC, p.TC, p.a, p.b);
   }
   wave_sort_pairs(key, bag, lane);
-  fill_base_table(tab, key, p, lane);
+  fill_base_table<SIGN>(tab, key, p, lane);
   const uint32_t prev = __shfl_up(key, 1);
   uint64_t starts = __ballot(lane < nb && (lane == 0 || prev != key));
   while (starts) {
@@ -59,8 +72,9 @@ __device__ __forceinline__ void forward_onehot_tile(
       const int pu = pos[u] < nb ? pos[u] : pos[0];
 #pragma unroll
       for (int r = 0; r < EPL; ++r) {
-        const uint32_t m = act[r] ? wrap_add(tab[pu * kTabStride + jj[r]], kk[r], p.M) : 0u;
-        v[u][r] = load_weight(w, m);
+        const Elem el = elem_of<SIGN>(tab[pu * kTabStride + jj[r]], kk[r], p.M);
+        const float x = load_weight(w, act[r] ? el.m : 0u);
+        v[u][r] = SIGN ? apply_sign(x, el) : x;
       }
     }
 #pragma unroll
@@ -70,16 +84,16 @@ __device__ __forceinline__ void forward_onehot_tile(
         const uint64_t ro = readlane_u64(tl.row_off, b) + c0 + lane;
 #pragma unroll
         for (int r = 0; r < EPL; ++r)
-          if (act[r]) __builtin_nontemporal_store(v[u][r], out + ro + kWave * r);
+          if (act[r]) store_out(out, ro + kWave * r, v[u][r], p.rows_bf16);
       }
     }
   }
 }
 
-template <typename WT, int EPL, int U, bool TAB>
+template <typename WT, int EPL, int U, bool TAB, bool SIGN>
 __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
-    const WT* __restrict__ w, const KParams p, const int64_t* __restrict__ indices,
-    const int64_t* __restrict__ offsets, float* __restrict__ out) {
+    const WT* __restrict__ w, const KParams p, const void* __restrict__ indices,
+    const void* __restrict__ offsets, void* __restrict__ out) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
   const uint64_t g0 = wave * kTileBags;
@@ -89,7 +103,7 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
   __shared__ uint32_t tab_all[TAB ? kWavesPerBlock * kWave * kTabStride : 1];
   uint32_t* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabStride : 0);
 
-  uint32_t step[EPL], kk[EPL], jj[EPL];
+  uint32_t step[EPL], step2[EPL], kk[EPL], jj[EPL];
   bool act[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) {
@@ -99,6 +113,7 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     jj[r] = cc / p.Z;
     kk[r] = cc - jj[r] * p.Z;
     step[r] = TAB ? 0u : chunk_step(p.a, jj[r]);
+    step2[r] = (TAB || !SIGN) ? 0u : chunk_step(p.a2, jj[r]);
   }
 
   const Tile tl = load_tile(p, offsets, g0, lane);
@@ -106,10 +121,8 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
   if (TAB) {
     // One-hot tile (every bag exactly one item): gather each distinct token
     // of the tile once and store its row to every bag that reads it.
-    const int64_t nxt = __shfl_down(tl.start, 1);
-    const int64_t end = lane == tl.nb - 1 ? tl.E1 : nxt;
-    if (__ballot(lane >= tl.nb || end - tl.start == 1) == ~0ull) {
-      forward_onehot_tile<WT, EPL, U>(w, p, tl, indices, out, tab, lane, c0, jj, kk, act);
+    if (__ballot(lane >= tl.nb || tl.len == 1) == ~0ull) {
+      forward_onehot_tile<WT, EPL, U, SIGN>(w, p, tl, indices, out, tab, lane, c0, jj, kk, act);
       return;
     }
   }
@@ -121,9 +134,15 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
 
   auto store_row = [&](int bag, bool zero) {
     const uint64_t ro = readlane_u64(tl.row_off, bag) + c0 + lane;
+    float div = 1.f;
+    if (p.mean && !zero) div = static_cast<float>(readlane_u32(tl.len, bag));
 #pragma unroll
-    for (int r = 0; r < EPL; ++r)
-      if (act[r]) __builtin_nontemporal_store(zero ? 0.f : acc[r], out + ro + kWave * r);
+    for (int r = 0; r < EPL; ++r) {
+      if (act[r]) {
+        const float x = zero ? 0.f : (p.mean ? acc[r] / div : acc[r]);
+        store_out(out, ro + kWave * r, x, p.rows_bf16);
+      }
+    }
   };
 
   for (int64_t blk = tl.E0; blk < tl.E1; blk += kWave) {
@@ -131,10 +150,10 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     const int n = rem < kWave ? static_cast<int>(rem) : kWave;
     const int64_t e = blk + lane;
     uint32_t idx = 0;
-    if (lane < n) idx = static_cast<uint32_t>(__builtin_nontemporal_load(indices + e));
+    if (lane < n) idx = load_index(indices, e, p.idx32);
     const int bag = bag_of_item(tl, e);
     const uint32_t tC = __shfl(tl.tC, bag);
-    if (TAB) fill_base_table(tab, item_hash(idx, tC, p.TC, p.a, p.b), p, lane);
+    if (TAB) fill_base_table<SIGN>(tab, item_hash(idx, tC, p.TC, p.a, p.b), p, lane);
 
     for (int q = 0; q < n; q += U) {
       // Gather phase: straight-line, U items x EPL loads in flight.  Items
@@ -144,14 +163,20 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int uu = q + u < n ? q + u : n - 1;
-        uint32_t h0 = 0;
-        if (!TAB) h0 = item_hash(readlane_u32(idx, uu), readlane_u32(tC, uu), p.TC, p.a, p.b);
+        uint32_t h0 = 0, h20 = 0;
+        if (!TAB) {
+          h0 = item_hash(readlane_u32(idx, uu), readlane_u32(tC, uu), p.TC, p.a, p.b);
+          if (SIGN) h20 = sign_hash0(h0, p.s_alpha, p.s_beta);
+        }
 #pragma unroll
         for (int r = 0; r < EPL; ++r) {
-          const uint32_t base = TAB ? tab[uu * kTabStride + jj[r]]
-                                    : fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M);
-          const uint32_t m = act[r] ? wrap_add(base, kk[r], p.M) : 0u;
-          v[u][r] = load_weight(w, m);
+          const uint32_t ent =
+              TAB ? tab[uu * kTabStride + jj[r]]
+                  : chunk_entry<SIGN>(fast_mod(add_mod_p(h0, step[r]), p.fm_c, p.M),
+                                      add_mod_p(h20, step2[r]), p);
+          const Elem el = elem_of<SIGN>(ent, kk[r], p.M);
+          const float x = load_weight(w, act[r] ? el.m : 0u);
+          v[u][r] = SIGN ? apply_sign(x, el) : x;
         }
       }
       // Pool phase: stores only here, after every gather of the batch was
@@ -177,38 +202,45 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
   for (int z = cur + 1; z < tl.nb; ++z) store_row(z, true);
 }
 
-template <typename WT, int EPL, int U, bool TAB>
-static hipError_t launch_fwd_t(const WT* w, const KParams& p, const int64_t* indices,
-                               const int64_t* offsets, float* out, hipStream_t stream) {
+template <typename WT, int EPL, int U, bool TAB, bool SIGN>
+static hipError_t launch_fwd_t(const WT* w, const KParams& p, const void* indices,
+                               const void* offsets, void* out, hipStream_t stream) {
   const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
   const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
   if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
   dim3 grid(static_cast<uint32_t>(blocks), slabs);
-  hipLaunchKernelGGL((forward_kernel<WT, EPL, U, TAB>), grid, dim3(kBlockThreads), 0, stream, w, p,
-                     indices, offsets, out);
+  hipLaunchKernelGGL((forward_kernel<WT, EPL, U, TAB, SIGN>), grid, dim3(kBlockThreads), 0, stream,
+                     w, p, indices, offsets, out);
   return hipGetLastError();
 }
 
-template <typename WT, bool TAB>
-static hipError_t launch_fwd_c(const WT* w, const KParams& p, const int64_t* indices,
-                               const int64_t* offsets, float* out, hipStream_t stream) {
-  if (p.d <= 64) return launch_fwd_t<WT, 1, 16, TAB>(w, p, indices, offsets, out, stream);
-  if (p.d <= 128) return launch_fwd_t<WT, 2, 8, TAB>(w, p, indices, offsets, out, stream);
-  if (p.d <= 256) return launch_fwd_t<WT, 4, 4, TAB>(w, p, indices, offsets, out, stream);
-  return launch_fwd_t<WT, 8, 2, TAB>(w, p, indices, offsets, out, stream);
+template <typename WT, bool TAB, bool SIGN>
+static hipError_t launch_fwd_c(const WT* w, const KParams& p, const void* indices,
+                               const void* offsets, void* out, hipStream_t stream) {
+  if (p.d <= 64) return launch_fwd_t<WT, 1, 16, TAB, SIGN>(w, p, indices, offsets, out, stream);
+  if (p.d <= 128) return launch_fwd_t<WT, 2, 8, TAB, SIGN>(w, p, indices, offsets, out, stream);
+  if (p.d <= 256) return launch_fwd_t<WT, 4, 4, TAB, SIGN>(w, p, indices, offsets, out, stream);
+  return launch_fwd_t<WT, 8, 2, TAB, SIGN>(w, p, indices, offsets, out, stream);
+}
+
+template <typename WT, bool SIGN>
+static hipError_t launch_fwd_s(const WT* w, const KParams& p, const void* indices,
+                               const void* offsets, void* out, hipStream_t stream) {
+  if (p.C <= static_cast<uint32_t>(kTabChunks))
+    return launch_fwd_c<WT, true, SIGN>(w, p, indices, offsets, out, stream);
+  return launch_fwd_c<WT, false, SIGN>(w, p, indices, offsets, out, stream);
 }
 
 template <typename WT>
-static hipError_t launch_fwd_w(const WT* w, const KParams& p, const int64_t* indices,
-                               const int64_t* offsets, float* out, hipStream_t stream) {
-  if (p.C <= static_cast<uint32_t>(kTabChunks))
-    return launch_fwd_c<WT, true>(w, p, indices, offsets, out, stream);
-  return launch_fwd_c<WT, false>(w, p, indices, offsets, out, stream);
+static hipError_t launch_fwd_w(const WT* w, const KParams& p, const void* indices,
+                               const void* offsets, void* out, hipStream_t stream) {
+  if (p.sign_mode) return launch_fwd_s<WT, true>(w, p, indices, offsets, out, stream);
+  return launch_fwd_s<WT, false>(w, p, indices, offsets, out, stream);
 }
 
-hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const int64_t* indices,
-                          const int64_t* offsets, float* out, hipStream_t stream) {
+hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const void* indices,
+                          const void* offsets, void* out, hipStream_t stream) {
   if (bf16)
     return launch_fwd_w(static_cast<const uint16_t*>(w), p, indices, offsets, out, stream);
   return launch_fwd_w(static_cast<const float*>(w), p, indices, offsets, out, stream);

@@ -83,6 +83,41 @@ PSS_HD uint32_t wrap_add(uint32_t base, uint32_t k, uint32_t M) {
   return s >= M ? s - M : s;
 }
 
+// ---------------------------------------------------------------------------
+// Optional chunk sign (Sec. 2.5: entries of S that are +1, -1 or 0, drawn by
+// a universal hash).  A second hash of the same key, h2 = (a2 * key + b2)
+// mod p, gives the factor of chunk (i, j):
+//   mode 1 (+-1):   -1 if h2 >= 2^30, else +1
+//   mode 2 (+-1/0): +1 if h2 < q, -1 if q <= h2 < 2q, else 0, q = floor(p/6)
+// Kernels that only hold the item hash h_0 = (a * key_0 + b) mod p recover
+// the second hash from it: key_0 = (h_0 - b) * a^-1 (mod p), hence
+// h2_0 = alpha * h_0 + beta (mod p) with alpha = a2 * a^-1 and
+// beta = b2 - alpha * b; chunk j adds a2 * j (mod p) as for the location.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kQ6 = kP / 6;  // 357913941
+
+// Sign code of a chunk: 0 = +1, 1 = -1, 2 = not read (factor 0).
+PSS_HD uint32_t sign_code(uint32_t h2, uint32_t mode) {
+  if (mode == 1) return h2 >= (1u << 30) ? 1u : 0u;
+  return h2 < kQ6 ? 0u : (h2 < 2 * kQ6 ? 1u : 2u);
+}
+
+// h2_0 from the item hash h_0 (alpha, beta < p).
+PSS_HD uint32_t sign_hash0(uint32_t h0, uint32_t alpha, uint32_t beta) {
+  return mod_p(static_cast<uint64_t>(alpha) * h0 + beta);
+}
+
+// x^e mod p (host set-up of a^-1 = a^(p-2)).
+PSS_HD uint32_t pow_mod_p(uint32_t x, uint32_t e) {
+  uint32_t r = 1, b = x;
+  while (e) {
+    if (e & 1u) r = mod_p(static_cast<uint64_t>(r) * b);
+    b = mod_p(static_cast<uint64_t>(b) * b);
+    e >>= 1;
+  }
+  return r;
+}
+
 // Full chunk base h(i, j) = (((i*T + t)*C + j) * a + b mod p) mod M.
 PSS_HD uint32_t chunk_base(uint32_t i, uint32_t t, uint32_t j, uint32_t C, uint32_t TC,
                            uint32_t a, uint32_t b, uint64_t c, uint32_t M) {

@@ -32,8 +32,28 @@ struct KParams {
   uint32_t T, B;
   uint32_t C, Z, d;
   uint32_t TC;        // T*C (< 2^32)
-  uint32_t row_stride;  // T*d: floats per pooled row
+  uint32_t row_stride;  // T*d: elements per pooled row
+  // Options (pss_hash_params.flags).  sign_mode 0 = no sign; otherwise the
+  // chunk sign comes from h2_0 = (s_alpha * h_0 + s_beta) mod p plus
+  // a2 * j (mod p) for chunk j.
+  uint32_t sign_mode, s_alpha, s_beta, a2;
+  uint32_t mean;       // 1: mean pooling (each item weighs 1/|bag|)
+  uint32_t idx32;      // 1: indices and offsets are int32
+  uint32_t rows_bf16;  // 1: out / grad_out rows are bfloat16
 };
+
+// indices[e] / offsets[g] in either integer width (wave-uniform choice).
+__device__ __forceinline__ uint32_t load_index(const void* idx, int64_t e, uint32_t i32) {
+  return i32 ? static_cast<uint32_t>(
+                   __builtin_nontemporal_load(static_cast<const int32_t*>(idx) + e))
+             : static_cast<uint32_t>(
+                   __builtin_nontemporal_load(static_cast<const int64_t*>(idx) + e));
+}
+__device__ __forceinline__ int64_t load_offset(const void* off, uint64_t g, uint32_t i32) {
+  return i32 ? static_cast<int64_t>(
+                   __builtin_nontemporal_load(static_cast<const int32_t*>(off) + g))
+             : __builtin_nontemporal_load(static_cast<const int64_t*>(off) + g);
+}
 
 // bfloat16 bits <-> float
 __device__ __forceinline__ float bf16_to_f32(uint16_t v) {
@@ -47,6 +67,18 @@ PSS_HD uint16_t f32_to_bf16_rne(float f) {
   if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
   u += 0x7fffu + ((u >> 16) & 1u);
   return static_cast<uint16_t>(u >> 16);
+}
+
+// Gradient rows: float32 or bfloat16 bits, widened exactly.
+template <typename GT>
+__device__ __forceinline__ float load_row(const GT* g, uint64_t k);
+template <>
+__device__ __forceinline__ float load_row<float>(const float* g, uint64_t k) {
+  return __builtin_nontemporal_load(g + k);
+}
+template <>
+__device__ __forceinline__ float load_row<uint16_t>(const uint16_t* g, uint64_t k) {
+  return __uint_as_float(static_cast<uint32_t>(__builtin_nontemporal_load(g + k)) << 16);
 }
 
 template <typename WT>
@@ -74,20 +106,21 @@ struct Tile {
   int64_t start;      // lane l: first item of bag g0 + l (clamped, monotone)
   uint32_t tC;        // lane l: t * C of bag g0 + l
   uint64_t row_off;   // lane l: b * T*d + t*d of bag g0 + l
+  uint32_t len;       // lane l: number of items of bag g0 + l
 };
 
 // Loads the tile's offsets (one coalesced load) and per-bag constants.
 // Offsets are clamped to [0, N] and made monotone within the tile, so item
 // ranges never leave `indices` whatever the offsets array holds.
-__device__ __forceinline__ Tile load_tile(const KParams& p, const int64_t* __restrict__ offsets,
+__device__ __forceinline__ Tile load_tile(const KParams& p, const void* __restrict__ offsets,
                                           uint64_t g0, int lane) {
   Tile tl;
   tl.g0 = g0;
   const uint64_t left = p.num_bags - g0;
   tl.nb = left < static_cast<uint64_t>(kTileBags) ? static_cast<int>(left) : kTileBags;
   int64_t s = 0;
-  if (lane < tl.nb) s = __builtin_nontemporal_load(offsets + g0 + lane);
-  int64_t e_last = __builtin_nontemporal_load(offsets + g0 + tl.nb);
+  if (lane < tl.nb) s = load_offset(offsets, g0 + lane, p.idx32);
+  int64_t e_last = load_offset(offsets, g0 + tl.nb, p.idx32);
   s = s < 0 ? 0 : (s > p.N ? p.N : s);
   e_last = e_last < 0 ? 0 : (e_last > p.N ? p.N : e_last);
   // running max over lanes keeps starts monotone (inclusive scan of max)
@@ -102,6 +135,9 @@ __device__ __forceinline__ Tile load_tile(const KParams& p, const int64_t* __res
   const int64_t last_start = __shfl(s, tl.nb - 1);
   tl.E0 = first;
   tl.E1 = e_last < last_start ? last_start : e_last;
+  // items of bag g0 + lane: [start, next start) (the last bag ends at E1)
+  const int64_t nxt = __shfl_down(s, 1);
+  tl.len = lane < tl.nb ? static_cast<uint32_t>((lane == tl.nb - 1 ? tl.E1 : nxt) - s) : 0u;
   const uint64_t g = g0 + static_cast<uint64_t>(lane < tl.nb ? lane : 0);
   const uint32_t t = static_cast<uint32_t>(g / p.B);
   const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
@@ -118,13 +154,56 @@ __device__ __forceinline__ Tile load_tile(const KParams& p, const int64_t* __res
 constexpr int kTabChunks = 16;
 constexpr int kTabStride = kTabChunks + 1;  // padding against bank conflicts
 
+//
+// With a chunk sign the entry also carries it: base | 2^31 for -1, and
+// kSkip for a chunk that is not read (bases are below M <= 2^31 - 1, so
+// neither collides with a plain base).
+constexpr uint32_t kSkip = 0xffffffffu;
+
+template <bool SIGN>
+__device__ __forceinline__ uint32_t chunk_entry(uint32_t base, uint32_t h2, const KParams& p) {
+  if (!SIGN) return base;
+  const uint32_t code = sign_code(h2, p.sign_mode);
+  return code == 2u ? kSkip : base | (code << 31);
+}
+
+template <bool SIGN>
 __device__ __forceinline__ void fill_base_table(uint32_t* tab, uint32_t h0, const KParams& p,
                                                 int lane) {
   uint32_t step = 0;  // a * j mod p, j = 0 .. C-1
+  uint32_t h2 = SIGN ? sign_hash0(h0, p.s_alpha, p.s_beta) : 0u;
   for (uint32_t j = 0; j < p.C; ++j) {
-    tab[lane * kTabStride + j] = fast_mod(add_mod_p(h0, step), p.fm_c, p.M);
+    tab[lane * kTabStride + j] =
+        chunk_entry<SIGN>(fast_mod(add_mod_p(h0, step), p.fm_c, p.M), h2, p);
     step = add_mod_p(step, p.a);
+    if (SIGN) h2 = add_mod_p(h2, p.a2);
   }
+}
+
+// Element k of the chunk of table entry `ent`: its address (0 for a chunk
+// that is not read, so the load stays in bounds) and the float sign mask.
+struct Elem {
+  uint32_t m, neg;
+  bool read;
+};
+template <bool SIGN>
+__device__ __forceinline__ Elem elem_of(uint32_t ent, uint32_t k, uint32_t M) {
+  Elem e;
+  if (!SIGN) {
+    e.m = wrap_add(ent, k, M);
+    e.neg = 0;
+    e.read = true;
+    return e;
+  }
+  e.read = ent != kSkip;
+  e.neg = ent & 0x80000000u;
+  e.m = e.read ? wrap_add(ent & 0x7fffffffu, k, M) : 0u;
+  return e;
+}
+
+// x * (+1 or -1) by flipping the sign bit; a chunk that is not read gives 0.
+__device__ __forceinline__ float apply_sign(float x, const Elem& e) {
+  return e.read ? __uint_as_float(__float_as_uint(x) ^ e.neg) : 0.f;
 }
 
 // Bitonic sort of one (key, payload) pair per lane across the 64 lanes of a

@@ -9,25 +9,28 @@
 namespace pss {
 
 // Forward: pooled rows of every bag into out[B][T*d].
-hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const int64_t* indices,
-                          const int64_t* offsets, float* out, hipStream_t stream);
+// indices / offsets are int64 (int32 when p.idx32); out / grad rows are
+// float32 (bfloat16 when p.rows_bf16).
+hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const void* indices,
+                          const void* offsets, void* out, hipStream_t stream);
 
 // Atomic deposit: dst[addr] += scale * grad for every (item, dim).
-hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, const int64_t* indices,
-                                 const int64_t* offsets, const float* grad, hipStream_t stream);
+hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, const void* indices,
+                                 const void* offsets, const void* grad, hipStream_t stream);
 
 // Sorted deposit: lookups grouped by token (radix sort on the item hash),
 // gradient rows summed per token, one deposit of scale * sum per token and
-// wavefront.  `workspace` must hold sorted_workspace_bytes(p.N) bytes.
-size_t sorted_workspace_bytes(int64_t N);
-hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const int64_t* indices,
-                                 const int64_t* offsets, const float* grad, void* workspace,
+// wavefront.  `workspace` must hold sorted_workspace_bytes(p) bytes.
+size_t sorted_workspace_bytes(const KParams& p);
+hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,
+                                 const void* offsets, const void* grad, void* workspace,
                                  hipStream_t stream);
 
 // Building blocks of the sorted path, shared with the sparse-gradient path.
-// keygen: keys[e] = item part of the hash of lookup e, rows[e] = b*T + t.
-hipError_t launch_keygen(const KParams& p, const int64_t* indices, const int64_t* offsets,
-                         uint32_t* keys, uint32_t* rows, hipStream_t stream);
+// keygen: keys[e] = item part of the hash of lookup e, rows[e] = b*T + t;
+// with mean pooling also inv_len[b*T + t] = 1 / |bag| (nonempty bags).
+hipError_t launch_keygen(const KParams& p, const void* indices, const void* offsets,
+                         uint32_t* keys, uint32_t* rows, float* inv_len, hipStream_t stream);
 // Stable LSD radix sort of (keys, vals) by the low `bits` bits (8-bit
 // digits); on return keys/vals point at whichever buffer pair holds the
 // result.  scratch: radix_scratch_bytes(n) bytes.
@@ -40,10 +43,10 @@ int grouping_bits(int64_t N);
 // Sparse gradient (Alg. 1 sparse branch): ascending unique locations and
 // summed values into locations/values (at most `capacity` entries written),
 // their count into *num_unique32 (device).  workspace:
-// sparse_workspace_bytes(p) bytes.  Requires p.N * p.C < 2^32.
+// sparse_workspace_bytes(p) bytes.  Requires p.N * p.C < 2^31.
 size_t sparse_workspace_bytes(const KParams& p);
-hipError_t launch_gradient_sparse(const KParams& p, const int64_t* indices, const int64_t* offsets,
-                                  const float* grad, void* workspace, uint32_t* locations,
+hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const void* offsets,
+                                  const void* grad, void* workspace, uint32_t* locations,
                                   float* values, int64_t capacity, uint32_t* num_unique32,
                                   hipStream_t stream);
 hipError_t launch_store_count(const uint32_t* total, int64_t* out, hipStream_t stream);
@@ -61,8 +64,9 @@ hipError_t launch_optimizer(void* w, bool bf16, float* state, const float* G, in
 // captured into a graph).
 hipError_t launch_zero(float* dst, int64_t n, hipStream_t stream);
 
-// Chunk bases of every item into base_out[N][C].
-hipError_t launch_debug_addresses(const KParams& p, const int64_t* indices, const int64_t* offsets,
-                                  uint32_t* base_out, hipStream_t stream);
+// Chunk bases of every item into base_out[N][C] and/or sign factors
+// (+1, -1, 0) into sign_out[N][C] (either may be null).
+hipError_t launch_debug_addresses(const KParams& p, const void* indices, const void* offsets,
+                                  uint32_t* base_out, int8_t* sign_out, hipStream_t stream);
 
 }  // namespace pss

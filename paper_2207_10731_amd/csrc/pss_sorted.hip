@@ -35,9 +35,11 @@ static_assert(kBins % kBlockThreads == 0, "whole digits per thread in the scatte
 // ---------------------------------------------------------------------------
 // keygen
 // ---------------------------------------------------------------------------
+// With mean pooling it also writes inv_len[r] = 1 / |bag| for every pooled
+// row r = b*T + t of a nonempty bag (each bag belongs to exactly one tile).
 __global__ __launch_bounds__(kBlockThreads) void keygen_kernel(
-    const KParams p, const int64_t* __restrict__ indices, const int64_t* __restrict__ offsets,
-    uint32_t* __restrict__ keys, uint32_t* __restrict__ rows) {
+    const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
+    uint32_t* __restrict__ keys, uint32_t* __restrict__ rows, float* __restrict__ inv_len) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
   const uint64_t g0 = wave * kTileBags;
@@ -48,6 +50,7 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_kernel(
   const uint32_t t = static_cast<uint32_t>(g / p.B);
   const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
   const uint32_t rr = b * p.T + t;
+  if (p.mean && lane < tl.nb && tl.len) inv_len[rr] = 1.f / static_cast<float>(tl.len);
   for (int64_t blk = tl.E0; blk < tl.E1; blk += kWave) {
     const int64_t rem = tl.E1 - blk;
     const int n = rem < kWave ? static_cast<int>(rem) : kWave;
@@ -56,7 +59,7 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_kernel(
     const uint32_t tC = __shfl(tl.tC, bag);
     const uint32_t r = __shfl(rr, bag);
     if (lane < n) {
-      const uint32_t i = static_cast<uint32_t>(__builtin_nontemporal_load(indices + e));
+      const uint32_t i = load_index(indices, e, p.idx32);
       keys[e] = item_hash(i, tC, p.TC, p.a, p.b);
       rows[e] = r;
     }
@@ -200,11 +203,11 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
 // ---------------------------------------------------------------------------
 // segmented reduction + deposit
 // ---------------------------------------------------------------------------
-template <int EPL, int U, bool TAB>
+template <int EPL, int U, bool TAB, bool SIGN, typename GT>
 __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
     float* __restrict__ dst, const float scale, const KParams p,
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ rows,
-    const float* __restrict__ grad, const int64_t n) {
+    const GT* __restrict__ grad, const float* __restrict__ inv_len, const int64_t n) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6)) * kWave;
   if (p0 >= n) return;
@@ -213,7 +216,7 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
   __shared__ uint32_t tab_all[TAB ? kWavesPerBlock * kWave * kTabStride : 1];
   uint32_t* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabStride : 0);
 
-  uint32_t step[EPL], kk[EPL], jj[EPL];
+  uint32_t step[EPL], step2[EPL], kk[EPL], jj[EPL];
   bool act[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) {
@@ -223,6 +226,7 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
     jj[r] = cc / p.Z;
     kk[r] = cc - jj[r] * p.Z;
     step[r] = TAB ? 0u : chunk_step(p.a, jj[r]);
+    step2[r] = (TAB || !SIGN) ? 0u : chunk_step(p.a2, jj[r]);
   }
   uint32_t key = 0xffffffffu, row = 0;
   if (lane < cnt) {
@@ -236,7 +240,7 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
   // Empty lanes hold key 0xffffffff (> any hash) and stay at the end.
   wave_sort_pairs(key, row, lane);
   // lane l: chunk bases of the key it holds after the sort
-  if (TAB) fill_base_table(tab, key, p, lane);
+  if (TAB) fill_base_table<SIGN>(tab, key, p, lane);
   float acc[EPL];
 #pragma unroll
   for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
@@ -248,10 +252,14 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int uu = q + u < cnt ? q + u : cnt - 1;
-      const float* grow = grad + static_cast<uint64_t>(readlane_u32(row, uu)) * p.d;
+      const uint32_t ru = readlane_u32(row, uu);
+      const GT* grow = grad + static_cast<uint64_t>(ru) * p.d;
+      const float il = p.mean ? inv_len[ru] : 1.f;
 #pragma unroll
-      for (int r = 0; r < EPL; ++r)
-        gv[u][r] = __builtin_nontemporal_load(grow + (act[r] ? c0 + lane + kWave * r : 0u));
+      for (int r = 0; r < EPL; ++r) {
+        const float x = load_row(grow, act[r] ? c0 + lane + kWave * r : 0u);
+        gv[u][r] = p.mean ? x * il : x;
+      }
     }
     // Reduce phase: deposits (atomics) only after every load of the batch
     // was issued; loads and atomics share one wait counter on gfx9.
@@ -263,12 +271,17 @@ __global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
         const uint32_t h = readlane_u32(key, q + u);
         const uint32_t hn = q + u + 1 < cnt ? readlane_u32(key, q + u + 1) : ~h;
         if (hn != h) {
+          const uint32_t h20 = (!TAB && SIGN) ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
 #pragma unroll
           for (int r = 0; r < EPL; ++r) {
             if (act[r]) {
-              const uint32_t base = TAB ? tab[(q + u) * kTabStride + jj[r]]
-                                        : fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M);
-              unsafeAtomicAdd(dst + wrap_add(base, kk[r], p.M), scale * acc[r]);
+              const uint32_t ent =
+                  TAB ? tab[(q + u) * kTabStride + jj[r]]
+                      : chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M),
+                                          add_mod_p(h20, step2[r]), p);
+              const Elem el = elem_of<SIGN>(ent, kk[r], p.M);
+              if (!SIGN || el.read)
+                unsafeAtomicAdd(dst + el.m, SIGN ? apply_sign(scale * acc[r], el) : scale * acc[r]);
             }
             acc[r] = 0.f;
           }
@@ -283,8 +296,10 @@ size_t radix_scratch_bytes(int64_t n) {
   return (nblocks * kBins + kBins) * 4 + 256;
 }
 
-size_t sorted_workspace_bytes(int64_t N) {
-  return static_cast<size_t>(N) * 16 + radix_scratch_bytes(N);
+size_t sorted_workspace_bytes(const KParams& p) {
+  size_t s = static_cast<size_t>(p.N) * 16 + radix_scratch_bytes(p.N);
+  if (p.mean) s += (p.num_bags * 4 + 255) & ~uint64_t(255);
+  return s;
 }
 
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
@@ -322,37 +337,57 @@ int grouping_bits(int64_t N) {
   return bits;
 }
 
-hipError_t launch_keygen(const KParams& p, const int64_t* indices, const int64_t* offsets,
-                         uint32_t* keys, uint32_t* rows, hipStream_t stream) {
+hipError_t launch_keygen(const KParams& p, const void* indices, const void* offsets,
+                         uint32_t* keys, uint32_t* rows, float* inv_len, hipStream_t stream) {
   const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
   const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
   hipLaunchKernelGGL(keygen_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kBlockThreads), 0,
-                     stream, p, indices, offsets, keys, rows);
+                     stream, p, indices, offsets, keys, rows, inv_len);
   return hipGetLastError();
 }
 
-template <int EPL, int U, bool TAB>
+template <int EPL, int U, bool TAB, bool SIGN, typename GT>
 static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, const uint32_t* keys,
-                                  const uint32_t* rows, const float* grad, hipStream_t stream) {
+                                  const uint32_t* rows, const GT* grad, const float* inv_len,
+                                  hipStream_t stream) {
   const uint64_t waves = (static_cast<uint64_t>(p.N) + kWave - 1) / kWave;
   const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
-  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, TAB>), dim3(static_cast<uint32_t>(blocks), slabs),
-                     dim3(kBlockThreads), 0, stream, dst, scale, p, keys, rows, grad, p.N);
+  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, TAB, SIGN, GT>),
+                     dim3(static_cast<uint32_t>(blocks), slabs), dim3(kBlockThreads), 0, stream, dst,
+                     scale, p, keys, rows, grad, inv_len, p.N);
   return hipGetLastError();
 }
 
-template <bool TAB>
+template <bool TAB, bool SIGN, typename GT>
 static hipError_t launch_reduce_c(float* dst, float scale, const KParams& p, const uint32_t* keys,
-                                  const uint32_t* rows, const float* grad, hipStream_t stream) {
-  if (p.d <= 64) return launch_reduce_t<1, 16, TAB>(dst, scale, p, keys, rows, grad, stream);
-  if (p.d <= 128) return launch_reduce_t<2, 8, TAB>(dst, scale, p, keys, rows, grad, stream);
-  if (p.d <= 256) return launch_reduce_t<4, 4, TAB>(dst, scale, p, keys, rows, grad, stream);
-  return launch_reduce_t<8, 2, TAB>(dst, scale, p, keys, rows, grad, stream);
+                                  const uint32_t* rows, const GT* grad, const float* il,
+                                  hipStream_t stream) {
+  if (p.d <= 64) return launch_reduce_t<1, 16, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  if (p.d <= 128) return launch_reduce_t<2, 8, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  if (p.d <= 256) return launch_reduce_t<4, 4, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  return launch_reduce_t<8, 2, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
 }
 
-hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const int64_t* indices,
-                                 const int64_t* offsets, const float* grad, void* workspace,
+template <bool SIGN, typename GT>
+static hipError_t launch_reduce_s(float* dst, float scale, const KParams& p, const uint32_t* keys,
+                                  const uint32_t* rows, const GT* grad, const float* il,
+                                  hipStream_t stream) {
+  if (p.C <= static_cast<uint32_t>(kTabChunks))
+    return launch_reduce_c<true, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  return launch_reduce_c<false, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+}
+
+template <typename GT>
+static hipError_t launch_reduce_g(float* dst, float scale, const KParams& p, const uint32_t* keys,
+                                  const uint32_t* rows, const GT* grad, const float* il,
+                                  hipStream_t stream) {
+  if (p.sign_mode) return launch_reduce_s<true>(dst, scale, p, keys, rows, grad, il, stream);
+  return launch_reduce_s<false>(dst, scale, p, keys, rows, grad, il, stream);
+}
+
+hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,
+                                 const void* offsets, const void* grad, void* workspace,
                                  hipStream_t stream) {
   const int64_t N = p.N;
   if (N == 0) return hipSuccess;
@@ -361,11 +396,16 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   uint32_t* k1 = v0 + N;
   uint32_t* v1 = k1 + N;
   uint32_t* scratch = v1 + N;
-  hipError_t e = launch_keygen(p, indices, offsets, k0, v0, stream);
+  float* inv_len = p.mean ? reinterpret_cast<float*>(
+                                reinterpret_cast<char*>(scratch) + radix_scratch_bytes(N))
+                          : nullptr;
+  hipError_t e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);
   if (e == hipSuccess) e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), scratch, stream);
   if (e != hipSuccess) return e;
-  if (p.C <= static_cast<uint32_t>(kTabChunks)) return launch_reduce_c<true>(dst, scale, p, k0, v0, grad, stream);
-  return launch_reduce_c<false>(dst, scale, p, k0, v0, grad, stream);
+  if (p.rows_bf16)
+    return launch_reduce_g(dst, scale, p, k0, v0, static_cast<const uint16_t*>(grad), inv_len,
+                           stream);
+  return launch_reduce_g(dst, scale, p, k0, v0, static_cast<const float*>(grad), inv_len, stream);
 }
 
 }  // namespace pss

@@ -12,7 +12,9 @@
 //              floats) and its hash.
 //   chunks     one record (chunk base, run*C + j) per run and chunk, sorted
 //              by base (bases < M; unused records hold a sentinel base that
-//              sorts last).
+//              sorts last).  With a chunk sign, bit 31 of the record id marks
+//              a -1 chunk and chunks of factor 0 get the sentinel base (they
+//              read nothing, so they own and add nothing).
 //   merge      element m is owned by the last chunk, in base order, whose
 //              span [base, base + Z) covers it.  A chunk that runs past M
 //              wraps to 0: it is also entered, shifted by -M, in front of
@@ -126,11 +128,11 @@ __global__ __launch_bounds__(kBlockThreads) void piece_runs_kernel(uint32_t* __r
 }
 
 // Summed gradient row of every run; run slots from the scanned counts.
-template <int EPL, int U>
+template <int EPL, int U, typename GT>
 __global__ __launch_bounds__(kBlockThreads) void run_sums_kernel(
     const KParams p, const uint32_t* __restrict__ keys, const uint32_t* __restrict__ rows,
-    const int64_t n, const uint32_t* __restrict__ run_off, const float* __restrict__ grad,
-    float* __restrict__ rs, uint32_t* __restrict__ rk) {
+    const int64_t n, const uint32_t* __restrict__ run_off, const GT* __restrict__ grad,
+    const float* __restrict__ inv_len, float* __restrict__ rs, uint32_t* __restrict__ rk) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t piece = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
   const int64_t p0 = piece * kWave;
@@ -155,10 +157,14 @@ __global__ __launch_bounds__(kBlockThreads) void run_sums_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int uu = q + u < cnt ? q + u : cnt - 1;
-      const float* grow = grad + static_cast<uint64_t>(readlane_u32(row, uu)) * p.d;
+      const uint32_t ru = readlane_u32(row, uu);
+      const GT* grow = grad + static_cast<uint64_t>(ru) * p.d;
+      const float il = p.mean ? inv_len[ru] : 1.f;
 #pragma unroll
-      for (int r = 0; r < EPL; ++r)
-        gv[u][r] = __builtin_nontemporal_load(grow + (act[r] ? c0 + lane + kWave * r : 0u));
+      for (int r = 0; r < EPL; ++r) {
+        const float x = load_row(grow, act[r] ? c0 + lane + kWave * r : 0u);
+        gv[u][r] = p.mean ? x * il : x;
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -190,21 +196,36 @@ __global__ __launch_bounds__(kBlockThreads) void chunk_records_kernel(
   const int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
   if (x >= cap) return;
   const int64_t rc = static_cast<int64_t>(*num_runs) * p.C;
-  uint32_t b = 0xffffffffu;
+  uint32_t b = 0xffffffffu, id = static_cast<uint32_t>(x);
   if (x < rc) {
     const uint32_t r = static_cast<uint32_t>(x / p.C);
     const uint32_t j = static_cast<uint32_t>(x - static_cast<int64_t>(r) * p.C);
     b = fast_mod(add_mod_p(rk[r], chunk_step(p.a, j)), p.fm_c, p.M);
+    if (p.sign_mode) {
+      const uint32_t h2 = add_mod_p(sign_hash0(rk[r], p.s_alpha, p.s_beta), chunk_step(p.a2, j));
+      const uint32_t code = sign_code(h2, p.sign_mode);
+      if (code == 2u) b = 0xffffffffu;
+      id |= code << 31;  // code 1: negative (code 2 records are never read)
+    }
   }
   cb[x] = b;
-  cv[x] = static_cast<uint32_t>(x);
+  cv[x] = id;
 }
 
-// info[0] = number of chunk records RC, info[1] = records whose span wraps
-// (base > M - Z; a suffix of the sorted list).
+// info[0] = number of chunk records RC that read something (the sorted
+// records before the first sentinel), info[1] = records whose span wraps
+// (base > M - Z; a suffix of those RC).
 __global__ void tail_count_kernel(const KParams p, const uint32_t* __restrict__ cb,
                                   const uint32_t* __restrict__ num_runs, uint32_t* __restrict__ info) {
-  const uint64_t rc = static_cast<uint64_t>(*num_runs) * p.C;
+  uint64_t rc = static_cast<uint64_t>(*num_runs) * p.C;
+  {  // first sorted position holding the sentinel
+    uint64_t lo = 0, hi = rc;
+    while (lo < hi) {
+      const uint64_t mid = (lo + hi) / 2;
+      if (cb[mid] == 0xffffffffu) hi = mid; else lo = mid + 1;
+    }
+    rc = lo;
+  }
   // first sorted position with base > M - Z
   uint64_t lo = 0, hi = rc;
   const uint32_t lim = p.M - p.Z;
@@ -276,8 +297,10 @@ __global__ __launch_bounds__(kBlockThreads) void emit_kernel(
       const int64_t by = e.base(static_cast<uint32_t>(y));
       if (by + p.Z <= m) break;
       const uint32_t rec = cv[e.sorted_index(static_cast<uint32_t>(y))];
-      const uint32_t run = rec / p.C, j = rec - run * p.C;
-      v += rs[static_cast<uint64_t>(run) * p.d + j * p.Z + static_cast<uint32_t>(m - by)];
+      const uint32_t id = rec & 0x7fffffffu;
+      const uint32_t run = id / p.C, j = id - run * p.C;
+      const float x = rs[static_cast<uint64_t>(run) * p.d + j * p.Z + static_cast<uint32_t>(m - by)];
+      v += (rec >> 31) ? -x : x;
     }
     if (static_cast<int64_t>(out) < capacity) {
       locations[out] = static_cast<uint32_t>(m);
@@ -294,7 +317,7 @@ __global__ void store_count_kernel(const uint32_t* __restrict__ total, int64_t* 
 // host side
 // ---------------------------------------------------------------------------
 
-// Records have 32-bit ids: N*C must stay below 2^32.
+// Records have 31-bit ids (bit 31 carries the sign): N*C must stay below 2^31.
 static int64_t record_cap(const KParams& p) { return p.N * static_cast<int64_t>(p.C); }
 
 static int base_bits(uint32_t M) {  // smallest multiple of 8 with 2^bits > M
@@ -312,6 +335,7 @@ size_t sparse_workspace_bytes(const KParams& p) {
   s += static_cast<size_t>(N) * p.d * 4 + static_cast<size_t>(N) * 4;  // run sums + keys
   s += static_cast<size_t>(cap) * 16 + radix_scratch_bytes(cap);  // chunk records
   s += static_cast<size_t>(cap2) * 4 + scan_scratch_bytes(cap2) + 16;  // ownership
+  if (p.mean) s += static_cast<size_t>(p.num_bags) * 4;  // 1 / |bag| per pooled row
   return s + 64 * 16;  // alignment slack
 }
 
@@ -322,23 +346,34 @@ static T* carve(char*& cur, size_t count) {
   return p;
 }
 
-template <int EPL, int U>
-static void launch_run_sums(const KParams& p, const uint32_t* keys, const uint32_t* rows,
-                            const uint32_t* run_off, const float* grad, float* rs, uint32_t* rk,
-                            hipStream_t stream) {
+template <int EPL, int U, typename GT>
+static void launch_run_sums_t(const KParams& p, const uint32_t* keys, const uint32_t* rows,
+                              const uint32_t* run_off, const GT* grad, const float* inv_len,
+                              float* rs, uint32_t* rk, hipStream_t stream) {
   const uint64_t waves = (static_cast<uint64_t>(p.N) + kWave - 1) / kWave;
   const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
-  hipLaunchKernelGGL((run_sums_kernel<EPL, U>), dim3(static_cast<uint32_t>(blocks), slabs),
-                     dim3(kBlockThreads), 0, stream, p, keys, rows, p.N, run_off, grad, rs, rk);
+  hipLaunchKernelGGL((run_sums_kernel<EPL, U, GT>), dim3(static_cast<uint32_t>(blocks), slabs),
+                     dim3(kBlockThreads), 0, stream, p, keys, rows, p.N, run_off, grad, inv_len,
+                     rs, rk);
+}
+
+template <typename GT>
+static void launch_run_sums(const KParams& p, const uint32_t* keys, const uint32_t* rows,
+                            const uint32_t* run_off, const GT* grad, const float* inv_len,
+                            float* rs, uint32_t* rk, hipStream_t stream) {
+  if (p.d <= 64) launch_run_sums_t<1, 16>(p, keys, rows, run_off, grad, inv_len, rs, rk, stream);
+  else if (p.d <= 128) launch_run_sums_t<2, 8>(p, keys, rows, run_off, grad, inv_len, rs, rk, stream);
+  else if (p.d <= 256) launch_run_sums_t<4, 4>(p, keys, rows, run_off, grad, inv_len, rs, rk, stream);
+  else launch_run_sums_t<8, 2>(p, keys, rows, run_off, grad, inv_len, rs, rk, stream);
 }
 
 static uint32_t blocks_for(int64_t n) {
   return static_cast<uint32_t>((n + kBlockThreads - 1) / kBlockThreads);
 }
 
-hipError_t launch_gradient_sparse(const KParams& p, const int64_t* indices, const int64_t* offsets,
-                                  const float* grad, void* workspace, uint32_t* locations,
+hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const void* offsets,
+                                  const void* grad, void* workspace, uint32_t* locations,
                                   float* values, int64_t capacity, uint32_t* num_unique32,
                                   hipStream_t stream) {
   const int64_t N = p.N, cap = record_cap(p), cap2 = 2 * cap;
@@ -362,18 +397,19 @@ hipError_t launch_gradient_sparse(const KParams& p, const int64_t* indices, cons
   uint32_t* own = carve<uint32_t>(cur, cap2);
   uint32_t* oscr = carve<uint32_t>(cur, scan_scratch_bytes(cap2) / 4 + 1);
   uint32_t* info = carve<uint32_t>(cur, 4);
+  float* inv_len = p.mean ? carve<float>(cur, p.num_bags) : nullptr;
 
-  hipError_t e = launch_keygen(p, indices, offsets, k0, v0, stream);
+  hipError_t e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);
   if (e == hipSuccess) e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), rscr, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(piece_runs_kernel, dim3(static_cast<uint32_t>((npieces + kWavesPerBlock - 1) / kWavesPerBlock)),
                      dim3(kBlockThreads), 0, stream, k0, v0, N, runs);
   e = exclusive_scan(runs, npieces, sscr, num_runs, stream);
   if (e != hipSuccess) return e;
-  if (p.d <= 64) launch_run_sums<1, 16>(p, k0, v0, runs, grad, rs, rk, stream);
-  else if (p.d <= 128) launch_run_sums<2, 8>(p, k0, v0, runs, grad, rs, rk, stream);
-  else if (p.d <= 256) launch_run_sums<4, 4>(p, k0, v0, runs, grad, rs, rk, stream);
-  else launch_run_sums<8, 2>(p, k0, v0, runs, grad, rs, rk, stream);
+  if (p.rows_bf16)
+    launch_run_sums(p, k0, v0, runs, static_cast<const uint16_t*>(grad), inv_len, rs, rk, stream);
+  else
+    launch_run_sums(p, k0, v0, runs, static_cast<const float*>(grad), inv_len, rs, rk, stream);
   hipLaunchKernelGGL(chunk_records_kernel, dim3(blocks_for(cap)), dim3(kBlockThreads), 0, stream, p,
                      rk, num_runs, cap, cb, cv);
   e = hipGetLastError();

@@ -22,6 +22,9 @@ PSS_PRIME = 2**31 - 1
 PSS_F32, PSS_BF16 = 0, 1
 PSS_OK, PSS_ERR_INVALID_ARG, PSS_ERR_UNSUPPORTED, PSS_ERR_HIP, PSS_ERR_NO_MEMORY = 0, 1, 2, 3, 4
 PSS_BWD_AUTO, PSS_BWD_ATOMIC, PSS_BWD_SORTED, PSS_BWD_SPARSE = 0, 1, 2, 3
+PSS_BWD_MASK = 3
+PSS_SIGN_PM1, PSS_SIGN_SPARSE, PSS_SIGN_MASK = 1 << 2, 2 << 2, 3 << 2
+PSS_POOL_MEAN, PSS_INDEX_I32, PSS_ROWS_BF16 = 1 << 4, 1 << 5, 1 << 6
 
 
 class PssError(RuntimeError):
@@ -40,6 +43,8 @@ class pss_hash_params(ctypes.Structure):
         ("weight_dtype", ctypes.c_int32),
         ("eps", ctypes.c_float),
         ("flags", ctypes.c_uint32),
+        ("sign_a", ctypes.c_uint32),
+        ("sign_b", ctypes.c_uint32),
     ]
 
 
@@ -60,14 +65,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_forward.argtypes = [vp, i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_backward_update.argtypes = [vp, vp, i64, i32, i32, hp, vp, vp, vp, ctypes.c_float, vp]
     lib.pss_debug_addresses.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
+    lib.pss_debug_signs.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
+    lib.pss_hash_signs_host.argtypes = [i64, i32, i32, hp, vp, vp, vp]
     lib.pss_gradient_sparse.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp, vp, i64, vp, vp]
     lib.pss_hash_bases_host.argtypes = [i64, i32, i32, hp, vp, vp, vp]
     lib.pss_validate_offsets_host.argtypes = [vp, i64, i64]
     lib.pss_status_string.argtypes = [ctypes.c_int]
     lib.pss_status_string.restype = ctypes.c_char_p
     for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
-                 "pss_debug_addresses", "pss_gradient_sparse", "pss_hash_bases_host",
-                 "pss_validate_offsets_host"):
+                 "pss_debug_addresses", "pss_debug_signs", "pss_gradient_sparse",
+                 "pss_hash_bases_host", "pss_hash_signs_host", "pss_validate_offsets_host"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -116,18 +123,27 @@ def _need(t, dtype, name, device=True):
         raise ValueError(f"{name} must be a GPU tensor")
 
 
-def make_hash_params(seed=None, *, a=None, b=None, num_tables, batch, num_indices,
-                     weight_dtype=PSS_F32, eps=1e-10, flags=PSS_BWD_AUTO) -> pss_hash_params:
-    """Fills the parameter block; (a, b) from ``seed`` via pss_hash_params_from_seed."""
-    hp = pss_hash_params(0, 0, num_tables, batch, num_indices, weight_dtype, eps, flags)
+def make_hash_params(seed=None, *, a=None, b=None, sign_a=None, sign_b=None, num_tables, batch,
+                     num_indices, weight_dtype=PSS_F32, eps=1e-10,
+                     flags=PSS_BWD_AUTO) -> pss_hash_params:
+    """Fills the parameter block; (a, b, sign_a, sign_b) from ``seed`` via
+    pss_hash_params_from_seed, then any given explicitly."""
+    hp = pss_hash_params(0, 0, num_tables, batch, num_indices, weight_dtype, eps, flags, 1, 0)
     if seed is not None:
         _check(load_library().pss_hash_params_from_seed(ctypes.c_uint64(seed), ctypes.byref(hp)),
                "pss_hash_params_from_seed")
-    if a is not None:
-        hp.a = a
-    if b is not None:
-        hp.b = b
+    for name, v in (("a", a), ("b", b), ("sign_a", sign_a), ("sign_b", sign_b)):
+        if v is not None:
+            setattr(hp, name, v)
     return hp
+
+
+def _index_dtype(hp):
+    return torch.int32 if hp.flags & PSS_INDEX_I32 else torch.int64
+
+
+def _row_dtype(hp):
+    return torch.bfloat16 if hp.flags & PSS_ROWS_BF16 else torch.float32
 
 
 def _weight_dtype(shared):
@@ -141,9 +157,9 @@ def pss_forward(shared, M, Z, d, hash_params, indices, offsets, out, stream=None
         raise TypeError("shared must be float32 or bfloat16")
     if hash_params.weight_dtype != _weight_dtype(shared):
         raise TypeError("hash_params.weight_dtype does not match shared")
-    _need(indices, torch.int64, "indices")
-    _need(offsets, torch.int64, "offsets")
-    _need(out, torch.float32, "out")
+    _need(indices, _index_dtype(hash_params), "indices")
+    _need(offsets, _index_dtype(hash_params), "offsets")
+    _need(out, _row_dtype(hash_params), "out")
     _check(lib.pss_forward(_ptr(shared), M, Z, d, ctypes.byref(hash_params), _ptr(indices),
                            _ptr(offsets), _ptr(out), _stream(stream)), "pss_forward")
     return out
@@ -156,9 +172,9 @@ def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, g
     if hash_params.weight_dtype != _weight_dtype(shared):
         raise TypeError("hash_params.weight_dtype does not match shared")
     _need(state, torch.float32, "state")
-    _need(indices, torch.int64, "indices")
-    _need(offsets, torch.int64, "offsets")
-    _need(grad_out, torch.float32, "grad_out")
+    _need(indices, _index_dtype(hash_params), "indices")
+    _need(offsets, _index_dtype(hash_params), "offsets")
+    _need(grad_out, _row_dtype(hash_params), "grad_out")
     _check(lib.pss_backward_update(_ptr(shared), _ptr(state), M, Z, d, ctypes.byref(hash_params),
                                    _ptr(indices), _ptr(offsets), _ptr(grad_out),
                                    ctypes.c_float(lr), _stream(stream)), "pss_backward_update")
@@ -169,9 +185,9 @@ def pss_gradient_sparse(M, Z, d, hash_params, indices, offsets, grad_out, locati
     """locations: int32 tensor (uint32 bit patterns), values: float32, both of
     length >= min(M, N*d); num_unique: int64 tensor of one element."""
     lib = load_library()
-    _need(indices, torch.int64, "indices")
-    _need(offsets, torch.int64, "offsets")
-    _need(grad_out, torch.float32, "grad_out")
+    _need(indices, _index_dtype(hash_params), "indices")
+    _need(offsets, _index_dtype(hash_params), "offsets")
+    _need(grad_out, _row_dtype(hash_params), "grad_out")
     _need(locations, torch.int32, "locations")
     _need(values, torch.float32, "values")
     _need(num_unique, torch.int64, "num_unique")
@@ -185,13 +201,23 @@ def pss_gradient_sparse(M, Z, d, hash_params, indices, offsets, grad_out, locati
 
 def pss_debug_addresses(M, Z, d, hash_params, indices, offsets, base_out, stream=None):
     lib = load_library()
-    _need(indices, torch.int64, "indices")
-    _need(offsets, torch.int64, "offsets")
+    _need(indices, _index_dtype(hash_params), "indices")
+    _need(offsets, _index_dtype(hash_params), "offsets")
     _need(base_out, torch.int32, "base_out")  # uint32 bit patterns
     _check(lib.pss_debug_addresses(M, Z, d, ctypes.byref(hash_params), _ptr(indices),
                                    _ptr(offsets), _ptr(base_out), _stream(stream)),
            "pss_debug_addresses")
     return base_out
+
+
+def pss_debug_signs(M, Z, d, hash_params, indices, offsets, sign_out, stream=None):
+    lib = load_library()
+    _need(indices, _index_dtype(hash_params), "indices")
+    _need(offsets, _index_dtype(hash_params), "offsets")
+    _need(sign_out, torch.int8, "sign_out")
+    _check(lib.pss_debug_signs(M, Z, d, ctypes.byref(hash_params), _ptr(indices), _ptr(offsets),
+                               _ptr(sign_out), _stream(stream)), "pss_debug_signs")
+    return sign_out
 
 
 def pss_hash_bases_host(M, Z, d, hash_params, indices, offsets):
@@ -205,6 +231,20 @@ def pss_hash_bases_host(M, Z, d, hash_params, indices, offsets):
                                    idx.ctypes.data_as(ctypes.c_void_p),
                                    off.ctypes.data_as(ctypes.c_void_p),
                                    out.ctypes.data_as(ctypes.c_void_p)), "pss_hash_bases_host")
+    return out
+
+
+def pss_hash_signs_host(M, Z, d, hash_params, indices, offsets):
+    """Host evaluation of the library's chunk-sign code: int8 [N, C] of +1, -1, 0."""
+    import numpy as np
+    lib = load_library()
+    idx = np.ascontiguousarray(indices, dtype=np.int64)
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    out = np.zeros((idx.shape[0], d // Z if Z > 0 and d % Z == 0 else 1), dtype=np.int8)
+    _check(lib.pss_hash_signs_host(M, Z, d, ctypes.byref(hash_params),
+                                   idx.ctypes.data_as(ctypes.c_void_p),
+                                   off.ctypes.data_as(ctypes.c_void_p),
+                                   out.ctypes.data_as(ctypes.c_void_p)), "pss_hash_signs_host")
     return out
 
 
@@ -239,8 +279,10 @@ def compress_table(table, M, Z, hash_params, variant=PSS_BWD_SPARSE, out=None, s
 
     table: float32 [T, n, d] on the GPU.  Returns the float32 flat array of
     M elements whose element m is the sum of every table entry (t, i, c)
-    that the mapping sends to m (``out`` if given, which is overwritten).
-    Only (a, b) of ``hash_params`` are used.  One deposit pass of the
+    that the mapping sends to m (``out`` if given, which is overwritten),
+    times the chunk's sign factor when ``hash_params.flags`` selects a sign.
+    Only (a, b), the sign option and (sign_a, sign_b) of ``hash_params`` are
+    used.  One deposit pass of the
     library: every row is a one-item bag whose output gradient is the row,
     applied by SGD with lr = -1 to a zeroed array.  The default SPARSE
     backward sums each location in a fixed order (bitwise reproducible);
@@ -251,8 +293,9 @@ def compress_table(table, M, Z, hash_params, variant=PSS_BWD_SPARSE, out=None, s
     _need(table, torch.float32, "table")
     T, n, d = table.shape
     indices, offsets = _table_lookups(T, n, table.device)
+    sign = hash_params.flags & PSS_SIGN_MASK
     hp = pss_hash_params(hash_params.a, hash_params.b, 1, T * n, T * n, PSS_F32,
-                         hash_params.eps, variant)
+                         hash_params.eps, variant | sign, hash_params.sign_a, hash_params.sign_b)
     if out is None:
         out = torch.empty(M, dtype=torch.float32, device=table.device)
     _need(out, torch.float32, "out")
@@ -273,8 +316,10 @@ def lookup_rows(shared, M, Z, d, num_tables, rows, hash_params, stream=None):
     float32 [num_tables, rows, d] (one forward pass of one-item bags)."""
     T = num_tables
     indices, offsets = _table_lookups(T, rows, shared.device)
+    sign = hash_params.flags & PSS_SIGN_MASK
     hp = pss_hash_params(hash_params.a, hash_params.b, 1, T * rows, T * rows,
-                         _weight_dtype(shared), hash_params.eps, PSS_BWD_AUTO)
+                         _weight_dtype(shared), hash_params.eps, PSS_BWD_AUTO | sign,
+                         hash_params.sign_a, hash_params.sign_b)
     out = torch.empty((T, rows, d), dtype=torch.float32, device=shared.device)
     pss_forward(shared, M, Z, d, hp, indices, offsets, out.view(T * rows, d), stream)
     return out

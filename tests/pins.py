@@ -18,6 +18,9 @@ Every ``pin_*`` function raises AssertionError when the oracle module ``o``
   pin_sparse_dense       Alg. 1 sparse branch, densified, equals dense branch
   pin_untouched          elements no lookup reads stay bit-identical
   pin_bf16_rounding      nearest-even bfloat16 rounding == torch's
+  pin_sign_and_mean      sign variants and mean pooling against the signed
+                         sketch; torch's mean embedding_bag; SplitMix64
+                         outputs 2-4; factor frequencies
   pin_compress           post-hoc M = S E and (S e_i)^T M (Sec. 2.4, Thm. 2)
                          against the explicit S; the injective case; eps of
                          Def. 2 as a supremum; the distance bound of Thm. 1
@@ -343,6 +346,94 @@ def pin_compress(o, seed=10):
     assert np.all(o.pss_row_error(E, R) == 0)
 
 
+def pin_sign_and_mean(o, seed=11):
+    """Sign variants (Sec. 2.5 Achlioptas-type entries from a second hash)
+    and mean pooling against the pure-Python sketch with signed entries;
+    torch's mean embedding_bag in the injective case; the published
+    SplitMix64 stream behind (a2, b2); the frequencies of the factors."""
+    import torch
+    # SplitMix64 from state 0, outputs 2..4 (java.util.SplittableRandom(0))
+    assert o.splitmix64(0, 4)[1:] == [0x6E789E6AA1B965F4, 0x06C45D188009454F, 0xF88BB8A8724C81EC]
+    assert o.sign_params_from_seed(0) == (1 + 0x06C45D188009454F % (P - 1), 0xF88BB8A8724C81EC % P)
+    rng = np.random.default_rng(seed)
+    for k in range(36):
+        c = tiny_case(rng)
+        M, Z, d, T, B = c["M"], c["Z"], c["d"], c["T"], c["B"]
+        mode = [None, o.SIGN_PM1, o.SIGN_SPARSE][k % 3]
+        mean = bool((k // 3) % 2)
+        a2, b2 = int(rng.integers(1, P)), int(rng.integers(0, P))
+        sign = None if mode is None else (mode, a2, b2)
+        bsign = None if mode is None else (mode, a2, b2)
+        w = (rng.standard_normal(M) * 0.5).astype(np.float32)
+        got, s_abs = o.forward64(w, M, Z, d, T, B, c["a"], c["b"], c["indices"], c["offsets"],
+                                 sign=sign, mean=mean)
+        want = np.array(brute.forward(w, M, Z, d, T, B, c["rows"], c["a"], c["b"], c["indices"],
+                                      c["offsets"], sign=bsign, mean=mean))
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+        assert np.all(s_abs >= np.abs(got) - 1e-12)
+        g = rng.standard_normal((B, T * d)).astype(np.float32)
+        G, A, cnt = o.gradient_dense(M, Z, d, T, B, c["a"], c["b"], c["indices"], c["offsets"], g,
+                                     sign=sign, mean=mean)
+        Gw, cw = brute.gradient(M, Z, d, T, B, c["rows"], c["a"], c["b"], c["indices"],
+                                c["offsets"], g, sign=bsign, mean=mean)
+        np.testing.assert_allclose(G, Gw, rtol=1e-12, atol=1e-12)
+        loc, val = o.gradient_sparse(M, Z, d, T, B, c["a"], c["b"], c["indices"], c["offsets"], g,
+                                     sign=sign, mean=mean)
+        assert np.array_equal(loc, np.nonzero(cnt)[0])
+        np.testing.assert_allclose(val, G[loc], rtol=1e-12, atol=1e-12)
+        where = rng.choice(M, size=min(M, 9), replace=False)
+        Ga, Aa, ca = o.gradient_at(M, Z, d, T, B, c["a"], c["b"], c["indices"], c["offsets"], g,
+                                   where, sign=sign, mean=mean)
+        np.testing.assert_allclose(Ga, G[where], rtol=1e-12, atol=1e-12)
+        assert np.array_equal(ca, cnt[where])
+        # brute's reads count the zero entries of S too; the oracle drops them
+        if mode != o.SIGN_SPARSE:
+            assert np.array_equal(cnt, np.array(cw))
+        bags = rng.choice(T * B, size=min(T * B, 4), replace=False)
+        fa, _ = o.forward_at(w, M, Z, d, T, B, c["a"], c["b"], c["indices"], c["offsets"], bags,
+                             sign=sign, mean=mean)
+        full = got.reshape(B, T, d).transpose(1, 0, 2).reshape(T * B, d)
+        np.testing.assert_allclose(fa, full[bags], rtol=1e-12, atol=1e-12)
+    # factor frequencies over many keys: 1/2 each for pm1; 1/6, 1/6, 2/3 for sparse
+    n = 300_000
+    idx = rng.integers(0, 2**31, n)
+    t = rng.integers(0, 26, n)
+    for mode, want in ((o.SIGN_PM1, {1: 0.5, -1: 0.5, 0: 0.0}),
+                       (o.SIGN_SPARSE, {1: 1 / 6, -1: 1 / 6, 0: 2 / 3})):
+        f = o.signs_for(1, 4, 26, 987654321, 123456789, idx, t, mode)
+        for v, frac in want.items():
+            assert abs((f == v).mean() - frac) < 0.004, (mode, v, (f == v).mean())
+        # independent of the location hash: factor vs low bit of the base
+        base = o.bases_for(4096, 1, 4, 26, 55555, 777, idx, t)
+        for v, frac in want.items():
+            if frac:
+                both = ((f == v) & (base % np.uint64(2) == 0)).mean()
+                assert abs(both - frac / 2) < 0.004
+    # injective layout: mean pooling == torch embedding_bag(mode="mean"),
+    # and its weight gradient
+    T, d, B, nr = 3, 8, 5, 7
+    M = nr * T * d + 5
+    lens = rng.integers(0, 4, T * B)
+    offsets = np.zeros(T * B + 1, dtype=np.int64)
+    np.cumsum(lens, out=offsets[1:])
+    idx = rng.integers(0, nr, int(offsets[-1])).astype(np.int64)
+    w = rng.uniform(-1, 1, M).astype(np.float32)
+    grad = rng.standard_normal((B, T * d)).astype(np.float32)
+    table = torch.tensor(w[: nr * T * d].astype(np.float64).reshape(nr * T, d), requires_grad=True)
+    t_of_item = np.repeat(np.arange(T * B) // B, lens)
+    rows = torch.tensor(idx * T + t_of_item)
+    pooled = torch.nn.functional.embedding_bag(rows, table, torch.tensor(offsets[:-1]), mode="mean")
+    want = pooled.detach().numpy().reshape(T, B, d).transpose(1, 0, 2).reshape(B, T * d)
+    got, _ = o.forward64(w, M, d, d, T, B, d, 0, idx, offsets, mean=True)
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-15)
+    g_t = torch.tensor(grad.astype(np.float64).reshape(B, T, d).transpose(1, 0, 2).reshape(T * B, d))
+    (pooled * g_t).sum().backward()
+    G, _, _ = o.gradient_dense(M, d, d, T, B, d, 0, idx, offsets, grad, mean=True)
+    np.testing.assert_allclose(G[: nr * T * d], table.grad.numpy().reshape(-1), rtol=1e-12,
+                               atol=1e-15)
+    assert np.all(G[nr * T * d:] == 0)
+
+
 ALL_PINS = [pin_hash_vectors, pin_forward_brute, pin_gradient_brute, pin_integer_forward,
             pin_embedding_bag, pin_mass, pin_finite_difference, pin_sparse_dense,
-            pin_untouched, pin_bf16_rounding, pin_compress]
+            pin_untouched, pin_bf16_rounding, pin_compress, pin_sign_and_mean]

@@ -36,6 +36,42 @@ def test_status_strings(lib):
 def test_hash_params_from_seed_matches_oracle(seed):
     hp = pss.make_hash_params(seed, num_tables=1, batch=1, num_indices=0)
     assert (hp.a, hp.b) == o.hash_params_from_seed(seed)
+    assert (hp.sign_a, hp.sign_b) == o.sign_params_from_seed(seed)
+
+
+@pytest.mark.parametrize("mode", ["pm1", "sparse"])
+def test_host_signs_match_oracle(mode):
+    """The kernels' route to the sign (second hash recovered from the item
+    hash by an affine map mod p) against the oracle's direct evaluation."""
+    flag = pss.PSS_SIGN_PM1 if mode == "pm1" else pss.PSS_SIGN_SPARSE
+    rng = np.random.default_rng(11)
+    for k in range(40):
+        M = int(rng.choice([1, 7, 4096, 2_500_000, 10**9, P]))
+        T = int(rng.choice([1, 3, 26]))
+        Z = min(int(rng.choice([1, 2, 4])), M)
+        d = Z * int(rng.choice([1, 2, 32]))
+        B = int(rng.integers(1, 6))
+        lens = rng.integers(0, 5, T * B)
+        off = np.zeros(T * B + 1, dtype=np.int64)
+        np.cumsum(lens, out=off[1:])
+        n = int(off[-1])
+        idx = rng.integers(0, 2**31, n).astype(np.int64)
+        if k % 5 == 0:
+            idx[: n // 2] = rng.choice([0, 1, P - 1, P, 2**31 - 1], n // 2)
+        a = int(rng.choice([1, 2, P - 1, int(rng.integers(1, P))]))
+        b = int(rng.choice([0, P - 1, int(rng.integers(0, P))]))
+        a2 = int(rng.choice([1, P - 1, int(rng.integers(1, P))]))
+        b2 = int(rng.choice([0, P - 1, int(rng.integers(0, P))]))
+        hp = pss.make_hash_params(a=a, b=b, sign_a=a2, sign_b=b2, num_tables=T, batch=B,
+                                  num_indices=n, flags=flag)
+        got = pss.pss_hash_signs_host(M, Z, d, hp, idx, off)
+        _, t, _ = o.item_bags(T, B, off)
+        want = o.signs_for(Z, d, T, a2, b2, idx, t, mode)
+        assert np.array_equal(got.astype(np.int64), want), (k, a, b, a2, b2)
+    # without a sign option every factor is +1
+    hp = pss.make_hash_params(3, num_tables=1, batch=2, num_indices=3)
+    assert np.all(pss.pss_hash_signs_host(64, 4, 8, hp, np.array([1, 2, 3]),
+                                          np.array([0, 1, 3])) == 1)
 
 
 def _host_bases(M, Z, d, T, B, a, b, idx, off):
@@ -93,10 +129,11 @@ def test_host_fast_mod(M):
 
 
 def _bad_call(lib, **kw):
-    args = dict(M=4096, Z=4, d=16, a=5, b=7, T=4, B=2, N=8, dtype=0, flags=0, eps=1e-10)
+    args = dict(M=4096, Z=4, d=16, a=5, b=7, T=4, B=2, N=8, dtype=0, flags=0, eps=1e-10,
+                sign_a=3, sign_b=11)
     args.update(kw)
     hp = pss.pss_hash_params(args["a"], args["b"], args["T"], args["B"], args["N"], args["dtype"],
-                             args["eps"], args["flags"])
+                             args["eps"], args["flags"], args["sign_a"], args["sign_b"])
     dummy = ctypes.c_void_p(0x1000)  # never dereferenced: checks fail before any use
     return lib.pss_forward(kw.get("shared", dummy), args["M"], args["Z"], args["d"],
                            ctypes.byref(hp), dummy, dummy, dummy, None)
@@ -104,7 +141,11 @@ def _bad_call(lib, **kw):
 
 @pytest.mark.parametrize("kw", [dict(M=0), dict(M=2**31), dict(Z=0), dict(Z=5000, M=4096),
                                 dict(Z=3), dict(d=4097 * 4), dict(a=0), dict(a=P),
-                                dict(b=P), dict(T=0), dict(B=0), dict(N=-1), dict(flags=4),
+                                dict(b=P), dict(T=0), dict(B=0), dict(N=-1), dict(flags=1 << 7),
+                                dict(flags=3 << 2), dict(flags=pss.PSS_SIGN_PM1, sign_a=0),
+                                dict(flags=pss.PSS_SIGN_SPARSE, sign_a=P),
+                                dict(flags=pss.PSS_SIGN_PM1, sign_b=P),
+                                dict(flags=pss.PSS_INDEX_I32, N=2**31),
                                 dict(T=2**31, Z=1, d=2), dict(shared=None)])
 def test_forward_rejects_bad_arguments(lib, kw):
     assert _bad_call(lib, **kw) == pss.PSS_ERR_INVALID_ARG
@@ -125,7 +166,7 @@ def test_backward_rejects_bad_arguments(lib):
     hp_neg = pss.pss_hash_params(5, 7, 4, 2, 8, 0, -1.0, 0)
     assert f(dummy, dummy, 4096, 4, 16, ctypes.byref(hp_neg), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
-    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 4)
+    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 1 << 7)
     assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp4), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
 
@@ -139,7 +180,7 @@ def test_gradient_sparse_rejects_bad_arguments(lib):
              None) == pss.PSS_ERR_INVALID_ARG
     assert f(4096, 4, 16, ctypes.byref(hp), dummy, dummy, dummy, dummy, dummy, 128, None,
              None) == pss.PSS_ERR_INVALID_ARG
-    big = pss.pss_hash_params(5, 7, 4, 2, 2**31, 0, 1e-10, 0)  # N*C = 2^33
+    big = pss.pss_hash_params(5, 7, 4, 2, 2**30, 0, 1e-10, 0)  # N*C = 2^32
     assert f(4096, 4, 16, ctypes.byref(big), dummy, dummy, dummy, dummy, dummy, 4096, dummy,
              None) == pss.PSS_ERR_UNSUPPORTED
 

@@ -80,8 +80,9 @@ def _bf16_truncate(x):
 _orig_contrib = o._contributions
 
 
-def _gradient_last_write_wins(M, Z, d, T, B, a, b, indices, offsets, grad_out):
-    addr, g = _orig_contrib(M, Z, d, T, B, a, b, indices, offsets, grad_out)
+def _gradient_last_write_wins(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign=None,
+                              mean=False):
+    addr, g = _orig_contrib(M, Z, d, T, B, a, b, indices, offsets, grad_out, sign, mean)
     G = np.zeros(M)
     G[addr] = g                                                          # no accumulation
     A = np.zeros(M)
@@ -111,6 +112,32 @@ def _row_error_squared(E, R):
     return np.sum(D * D, axis=-1)                                        # sqrt dropped
 
 
+def _signs_threshold_third(Z, d, T, a2, b2, idx, t, mode):
+    f = _orig_signs(Z, d, T, a2, b2, idx, t, mode)
+    if mode != o.SIGN_SPARSE:
+        return f
+    C = d // Z
+    i = np.asarray(idx, dtype=np.int64).astype(np.uint64)
+    tt = np.asarray(t, dtype=np.int64).astype(np.uint64)
+    key = (i * np.uint64(T) + tt)[:, None] * np.uint64(C) + np.arange(C, dtype=np.uint64)[None, :]
+    h2 = ((np.uint64(a2) * (key % np.uint64(P)) + np.uint64(b2)) % np.uint64(P)).astype(np.int64)
+    q = P // 3                                                           # 1/3 instead of 1/6
+    return np.where(h2 < q, 1, np.where(h2 < 2 * q, -1, 0)).astype(np.int64)
+
+
+def _signs_per_item(Z, d, T, a2, b2, idx, t, mode):
+    f = _orig_signs(Z, d, T, a2, b2, idx, t, mode)
+    return np.repeat(f[:, :1], f.shape[1], axis=1)                       # chunk 0's sign for all
+
+
+def _item_scale_ignores_mean(T, B, offsets, mean):
+    return _orig_scale(T, B, offsets, False)
+
+
+_orig_signs = o.signs_for
+_orig_scale = o.item_scale
+
+
 MUTANTS = {
     "hash_drops_b": ("bases_for", _bases_drop_b),
     "key_swaps_table_and_token": ("bases_for", _bases_swapped_key),
@@ -125,6 +152,9 @@ MUTANTS = {
     "compress_overwrites": ("compress", _compress_overwrites),
     "recover_token_major": ("recover", _recover_token_major),
     "row_error_squared": ("pss_row_error", _row_error_squared),
+    "sparse_signs_at_one_third": ("signs_for", _signs_threshold_third),
+    "one_sign_per_item": ("signs_for", _signs_per_item),
+    "gradient_ignores_mean": ("item_scale", _item_scale_ignores_mean),
 }
 
 

@@ -126,7 +126,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c2")
-    ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted"])
+    ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted", "sparse"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -142,7 +142,7 @@ def main():
     dev = torch.device("cuda", 0)
     wl = synth.get(args.config)
     flags = {"auto": pss.PSS_BWD_AUTO, "atomic": pss.PSS_BWD_ATOMIC,
-             "sorted": pss.PSS_BWD_SORTED}[args.variant]
+             "sorted": pss.PSS_BWD_SORTED, "sparse": pss.PSS_BWD_SPARSE}[args.variant]
     dt_code = pss.PSS_BF16 if wl.weight_dtype == "bf16" else pss.PSS_F32
 
     t0 = time.perf_counter()

@@ -1,0 +1,117 @@
+"""Full-size parity: every workload at its real size, through the same entry
+points and launch configuration that bench.py times (default backward
+variant), checked on sampled outputs the oracle evaluates one by one:
+pooled rows of sampled bags (forward_at) and updated weights at sampled
+elements of the shared array (gradient_at), half of them elements that the
+batch reads."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import pss_oracle as o
+from paper_2207_10731_amd import pss
+
+pytestmark = pytest.mark.gpu
+
+FULL = ["c2", "c3", "c4", "c5"]
+RTOL = {"f32": 1e-5, "bf16": 1e-2}
+
+
+class Full:
+    def __init__(self, key):
+        print(f"full-size {key}: preparing inputs", flush=True)
+        self.wl = wl = synth.get(key)
+        self.x = synth.make_inputs(wl)
+        self.w = synth.make_weights(wl)
+        self.dev = torch.device("cuda", 0)
+        if wl.weight_dtype == "bf16":
+            self.shared = torch.from_numpy(self.w.view(np.int16)).to(self.dev).view(torch.bfloat16)
+        else:
+            self.shared = torch.from_numpy(self.w).to(self.dev)
+        self.state = torch.zeros(wl.M, device=self.dev) if wl.optimizer == "adagrad" else None
+        self.idx = torch.from_numpy(self.x.indices).to(self.dev)
+        self.off = torch.from_numpy(self.x.offsets).to(self.dev)
+        self.hp = pss.make_hash_params(
+            wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=self.x.N, eps=wl.eps,
+            weight_dtype=pss.PSS_BF16 if wl.weight_dtype == "bf16" else pss.PSS_F32)
+        self.a, self.b = self.hp.a, self.hp.b
+
+
+@pytest.mark.parametrize("key", FULL)
+def test_fullsize_forward_sampled_bags(key):
+    F = Full(key)
+    wl = F.wl
+    out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=F.dev)
+    print(f"full-size {key}: forward over {F.x.N} lookups", flush=True)
+    pss.pss_forward(F.shared, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, out)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(100)
+    nb = wl.T * wl.B
+    bags = np.unique(np.concatenate([rng.choice(nb, 300, replace=False),
+                                     [0, nb - 1, wl.B - 1, wl.B, nb - 64, nb - 65]]))
+    t, b = bags // wl.B, bags % wl.B
+    got = out.view(wl.B, wl.T, wl.d)[torch.from_numpy(b).to(F.dev), torch.from_numpy(t).to(F.dev)]
+    got = got.cpu().numpy().astype(np.float64)
+    ref, s_abs = o.forward_at(F.w, wl.M, wl.Z, wl.d, wl.T, wl.B, F.a, F.b, F.x.indices,
+                              F.x.offsets, bags, wl.weight_dtype)
+    bad = np.abs(got - ref) > 1e-5 * s_abs + 1e-30
+    assert not bad.any(), f"{bad.sum()} of {bad.size} sampled outputs out of tolerance"
+
+
+def _sample_elements(F, rng, n_read=1500, n_any=500):
+    wl = F.wl
+    e = rng.choice(F.x.N, size=min(n_read, F.x.N), replace=False)
+    _, t_all, _ = o.item_bags(wl.T, wl.B, F.x.offsets)
+    addr = o.addresses_from_bases(wl.M, wl.Z, o.bases_for(wl.M, wl.Z, wl.d, wl.T, F.a, F.b,
+                                                          F.x.indices[e], t_all[e]))
+    read = addr[np.arange(e.shape[0]), rng.integers(0, wl.d, e.shape[0])]
+    anyw = rng.integers(0, wl.M, n_any)
+    return np.unique(np.concatenate([read, anyw, [0, wl.M - 1]]))
+
+
+@pytest.mark.parametrize("key", FULL)
+def test_fullsize_backward_sampled_elements(key):
+    F = Full(key)
+    wl = F.wl
+    # N(0, 1) output gradient drawn on the device (seeded), copied to the
+    # host for the oracle
+    gen = torch.Generator(device=F.dev).manual_seed(wl.data_seed)
+    g = torch.randn((wl.B, wl.T * wl.d), device=F.dev, generator=gen)
+    grad = g.cpu().numpy()
+    print(f"full-size {key}: backward over {F.x.N} lookups", flush=True)
+    pss.pss_backward_update(F.shared, F.state, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, wl.lr)
+    torch.cuda.synchronize()
+    del g
+    where = _sample_elements(F, np.random.default_rng(200))
+    wh = torch.from_numpy(where).to(F.dev)
+    if wl.weight_dtype == "bf16":
+        w_gpu = F.shared.view(torch.int16)[wh].cpu().numpy().view(np.uint16)
+    else:
+        w_gpu = F.shared[wh].cpu().numpy()
+    print(f"full-size {key}: oracle at {where.shape[0]} elements", flush=True)
+    G, A, cnt = o.gradient_at(wl.M, wl.Z, wl.d, wl.T, wl.B, F.a, F.b, F.x.indices, F.x.offsets,
+                              grad, where)
+    assert (cnt > 0).sum() >= where.shape[0] // 2  # the read elements were sampled
+    rtol = RTOL[wl.weight_dtype]
+    w_old = F.w[where]
+    w_old64 = o.widen(w_old, wl.weight_dtype)
+    if F.state is None:
+        w_ref = o.sgd_update(w_old, G, wl.lr, wl.weight_dtype)
+        bound = np.abs(w_old64) + wl.lr * A
+        exempt = np.zeros(where.shape[0], dtype=bool)
+    else:
+        s_gpu = F.state[wh].cpu().numpy().astype(np.float64)
+        w_ref, s_ref = o.adagrad_update(w_old, np.zeros(where.shape[0], np.float32), G, wl.lr,
+                                        wl.eps, wl.weight_dtype)
+        assert np.all(np.abs(s_gpu - s_ref.astype(np.float64)) <= rtol * A * A + 1e-30)
+        bound = np.abs(w_old64) + wl.lr * A / (np.sqrt(s_ref.astype(np.float64)) + wl.eps)
+        exempt = np.abs(G) <= rtol * A  # first step from s = 0: sign of a cancelled sum
+    err = np.abs(o.widen(w_gpu, wl.weight_dtype) - o.widen(w_ref, wl.weight_dtype))
+    bad = (err > rtol * bound + 1e-30) & ~exempt
+    assert not bad.any(), f"{bad.sum()} of {where.shape[0]} sampled weights out of tolerance"
+    untouched = cnt == 0
+    if wl.weight_dtype == "bf16":
+        assert np.array_equal(w_gpu[untouched], w_old[untouched])
+    else:
+        assert np.array_equal(w_gpu[untouched].view(np.uint32), w_old[untouched].view(np.uint32))

@@ -1,8 +1,8 @@
 """GPU parity: the HIP library (through the C ABI) against the CPU oracle.
 
 Sizes are small enough for the oracle to finish in seconds but span many
-64-bag tiles with a ragged last tile; full-size workloads are checked on
-sampled outputs in test_gpu_fullsize.py.
+64-bag tiles with a ragged last tile; the workloads at full size are checked
+on sampled outputs in test_gpu_fullsize.py.
 """
 import numpy as np
 import pytest

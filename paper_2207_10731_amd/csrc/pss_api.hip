@@ -182,23 +182,16 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
 
   if (variant == PSS_BWD_SPARSE) {
-    // Alg. 1 sparse branch: unique locations + summed values, then the
-    // optimizer at those locations only.
-    const int64_t cap = sparse_capacity(M, p);
-    const size_t list_bytes = (static_cast<size_t>(cap) * 8 + 255) & ~size_t(255);
+    // Alg. 1 sparse branch: unique locations + summed values, with the
+    // optimizer applied at each location as it is summed.
     const size_t ws_bytes = pss::sparse_workspace_bytes(p);
     void* ws = nullptr;
-    st = scratch_alloc(&ws, list_bytes + 256 + ws_bytes, stream);
+    st = scratch_alloc(&ws, 256 + ws_bytes, stream);
     if (st != PSS_OK) return st;
-    uint32_t* loc = static_cast<uint32_t*>(ws);
-    float* val = reinterpret_cast<float*>(loc + cap);
-    uint32_t* count = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + list_bytes);
-    void* sws = static_cast<char*>(ws) + list_bytes + 256;
-    hipError_t e = pss::launch_gradient_sparse(p, indices, offsets, grad_out, sws, loc, val, cap,
-                                               count, stream);
-    if (e == hipSuccess)
-      e = pss::launch_sparse_optimizer(shared, bf16, state, loc, val, count, cap, lr,
-                                       hash_params->eps, stream);
+    uint32_t* count = static_cast<uint32_t*>(ws);
+    hipError_t e = pss::launch_sparse_update(p, indices, offsets, grad_out,
+                                             static_cast<char*>(ws) + 256, count, shared, bf16,
+                                             state, lr, hash_params->eps, stream);
     const hipError_t ef = hipFreeAsync(ws, stream);
     return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
   }

@@ -33,10 +33,12 @@ hipError_t launch_keygen(const KParams& p, const void* indices, const void* offs
                          uint32_t* keys, uint32_t* rows, float* inv_len, hipStream_t stream);
 // Stable LSD radix sort of (keys, vals) by the low `bits` bits (8-bit
 // digits); on return keys/vals point at whichever buffer pair holds the
-// result.  scratch: radix_scratch_bytes(n) bytes.
+// result.  scratch: radix_scratch_bytes(n) bytes.  With n_dev the number of
+// pairs is min(n, *n_dev) (read on the device; n sizes the launch).
 size_t radix_scratch_bytes(int64_t n);
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
-                            int64_t n, int bits, uint32_t* scratch, hipStream_t stream);
+                            int64_t n, int bits, uint32_t* scratch, hipStream_t stream,
+                            const uint32_t* n_dev = nullptr);
 // Bits of the item hash the grouping sort orders for N lookups.
 int grouping_bits(int64_t N);
 
@@ -50,10 +52,11 @@ hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const v
                                   float* values, int64_t capacity, uint32_t* num_unique32,
                                   hipStream_t stream);
 hipError_t launch_store_count(const uint32_t* total, int64_t* out, hipStream_t stream);
-// SGD / Adagrad applied at the listed unique locations only.
-hipError_t launch_sparse_optimizer(void* w, bool bf16, float* state, const uint32_t* loc,
-                                   const float* val, const uint32_t* count, int64_t capacity,
-                                   float lr, float eps, hipStream_t stream);
+// Same pipeline, but SGD / Adagrad is applied at each unique location in
+// place of writing the list (*num_unique32 still receives the count).
+hipError_t launch_sparse_update(const KParams& p, const void* indices, const void* offsets,
+                                const void* grad, void* workspace, uint32_t* num_unique32, void* w,
+                                bool bf16, float* state, float lr, float eps, hipStream_t stream);
 
 // Dense optimizer pass over the M elements of a gradient buffer G (G[m] == 0
 // leaves element m untouched).  state == nullptr selects SGD.

@@ -85,10 +85,24 @@ __device__ __forceinline__ uint64_t lanes_below(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (kWave - lane));
 }
 
+// Number of keys to sort: the host's count, or fewer when the caller keeps
+// the real count in device memory (the host count is then an upper bound).
+__device__ __forceinline__ int64_t live_count(int64_t n, const uint32_t* n_dev) {
+  if (n_dev == nullptr) return n;
+  const int64_t d = *n_dev;
+  return d < n ? d : n;
+}
+
 // counts[d * nblocks + blk] = number of keys of tile blk with digit d.
 __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
-    const uint32_t* __restrict__ keys, const int64_t n, const int shift,
-    uint32_t* __restrict__ counts, const uint32_t nblocks) {
+    const uint32_t* __restrict__ keys, int64_t n, const int shift,
+    uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t* __restrict__ n_dev) {
+  n = live_count(n, n_dev);
+  if (static_cast<int64_t>(blockIdx.x) * kSortTile >= n) {  // no live key in this tile
+    for (int d = threadIdx.x; d < kBins; d += kBlockThreads)
+      counts[static_cast<uint64_t>(d) * nblocks + blockIdx.x] = 0;
+    return;
+  }
   __shared__ uint32_t hist[kWavesPerBlock][kBins];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
@@ -134,9 +148,12 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __re
 // Stable scatter of one tile by digit into its global slots.
 __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
-    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, const int64_t n,
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
     const int shift, const uint32_t* __restrict__ offsets, const uint32_t nblocks,
-    const uint32_t* __restrict__ totals) {
+    const uint32_t* __restrict__ totals, const uint32_t* __restrict__ n_dev) {
+  n = live_count(n, n_dev);
+  // tiles wholly past the live keys hold nothing (their counts are zero)
+  if (static_cast<int64_t>(blockIdx.x) * kSortTile >= n) return;
   __shared__ uint32_t cur[kWavesPerBlock][kBins];
   __shared__ uint32_t wsum[kWavesPerBlock];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
@@ -303,18 +320,19 @@ size_t sorted_workspace_bytes(const KParams& p) {
 }
 
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
-                            int64_t n, int bits, uint32_t* scratch, hipStream_t stream) {
+                            int64_t n, int bits, uint32_t* scratch, hipStream_t stream,
+                            const uint32_t* n_dev) {
   if (n == 0) return hipSuccess;
   const uint32_t nblocks = static_cast<uint32_t>((n + kSortTile - 1) / kSortTile);
   uint32_t* counts = scratch;
   uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
   for (int shift = 0; shift < bits; shift += kSortBits) {
     hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys, n,
-                       shift, counts, nblocks);
+                       shift, counts, nblocks, n_dev);
     hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
                        nblocks, totals);
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys,
-                       vals, ktmp, vtmp, n, shift, counts, nblocks, totals);
+                       vals, ktmp, vtmp, n, shift, counts, nblocks, totals, n_dev);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     uint32_t* t = keys; keys = ktmp; ktmp = t;

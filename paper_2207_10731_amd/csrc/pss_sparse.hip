@@ -22,7 +22,9 @@
 //              a scan gives every owned element its output slot, so the
 //              locations come out ascending.  The value at m is the sum, over
 //              the chunks covering m, walked from the owner backwards, of the
-//              run-sum entry for m.
+//              run-sum entry for m (element-parallel, see emit_kernel).  The
+//              backward's SPARSE variant applies the optimizer there instead
+//              of writing the list.
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -32,9 +34,22 @@ constexpr int kScanTile = kBlockThreads * 16;
 // ---------------------------------------------------------------------------
 // device-wide exclusive scan of uint32 (three phases)
 // ---------------------------------------------------------------------------
+// Live length: n, or min(n, *n_dev) when the real length is on the device.
+__device__ __forceinline__ int64_t live_len(int64_t n, const uint32_t* n_dev) {
+  if (n_dev == nullptr) return n;
+  const int64_t d = *n_dev;
+  return d < n ? d : n;
+}
+
 __global__ __launch_bounds__(kBlockThreads) void scan_reduce_kernel(const uint32_t* __restrict__ in,
-                                                                    const int64_t n,
-                                                                    uint32_t* __restrict__ sums) {
+                                                                    int64_t n,
+                                                                    uint32_t* __restrict__ sums,
+                                                                    const uint32_t* __restrict__ n_dev) {
+  n = live_len(n, n_dev);
+  if (static_cast<int64_t>(blockIdx.x) * kScanTile >= n) {
+    if (threadIdx.x == 0) sums[blockIdx.x] = 0;
+    return;
+  }
   __shared__ uint32_t wsum[kWavesPerBlock];
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * 16;
   uint32_t s = 0;
@@ -62,8 +77,11 @@ __global__ __launch_bounds__(kBlockThreads) void scan_sums_kernel(uint32_t* __re
 }
 
 __global__ __launch_bounds__(kBlockThreads) void scan_apply_kernel(uint32_t* __restrict__ data,
-                                                                   const int64_t n,
-                                                                   const uint32_t* __restrict__ sums) {
+                                                                   int64_t n,
+                                                                   const uint32_t* __restrict__ sums,
+                                                                   const uint32_t* __restrict__ n_dev) {
+  n = live_len(n, n_dev);
+  if (static_cast<int64_t>(blockIdx.x) * kScanTile >= n) return;
   __shared__ uint32_t wsum[kWavesPerBlock];
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + threadIdx.x * 16;
   uint32_t v[16];
@@ -86,13 +104,16 @@ static size_t scan_scratch_bytes(int64_t n) {
   return ((static_cast<uint64_t>(n) + kScanTile - 1) / kScanTile + 1) * 4;
 }
 
-// data[0..n) <- exclusive prefix sums; *total <- sum.  n >= 1.
+// data[0..n') <- exclusive prefix sums; *total <- sum, with n' = n, or
+// min(n, *n_dev) when given (entries past n' are left as they are).  n >= 1.
 static hipError_t exclusive_scan(uint32_t* data, int64_t n, uint32_t* sums, uint32_t* total,
-                                 hipStream_t stream) {
+                                 hipStream_t stream, const uint32_t* n_dev = nullptr) {
   const uint32_t nsums = static_cast<uint32_t>((n + kScanTile - 1) / kScanTile);
-  hipLaunchKernelGGL(scan_reduce_kernel, dim3(nsums), dim3(kBlockThreads), 0, stream, data, n, sums);
+  hipLaunchKernelGGL(scan_reduce_kernel, dim3(nsums), dim3(kBlockThreads), 0, stream, data, n, sums,
+                     n_dev);
   hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kBlockThreads), 0, stream, sums, nsums, total);
-  hipLaunchKernelGGL(scan_apply_kernel, dim3(nsums), dim3(kBlockThreads), 0, stream, data, n, sums);
+  hipLaunchKernelGGL(scan_apply_kernel, dim3(nsums), dim3(kBlockThreads), 0, stream, data, n, sums,
+                     n_dev);
   return hipGetLastError();
 }
 
@@ -190,31 +211,35 @@ __global__ __launch_bounds__(kBlockThreads) void run_sums_kernel(
 
 // One (chunk base, run*C + j) record per run and chunk; records past the
 // last run hold the sentinel base 0xffffffff.
+// info[2] <- number of records (runs * C).  Grid-stride over the records
+// that exist (the launch is sized for the bound N * C).
 __global__ __launch_bounds__(kBlockThreads) void chunk_records_kernel(
     const KParams p, const uint32_t* __restrict__ rk, const uint32_t* __restrict__ num_runs,
-    const int64_t cap, uint32_t* __restrict__ cb, uint32_t* __restrict__ cv) {
-  const int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
-  if (x >= cap) return;
+    const int64_t cap, uint32_t* __restrict__ cb, uint32_t* __restrict__ cv,
+    uint32_t* __restrict__ info) {
   const int64_t rc = static_cast<int64_t>(*num_runs) * p.C;
-  uint32_t b = 0xffffffffu, id = static_cast<uint32_t>(x);
-  if (x < rc) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) info[2] = static_cast<uint32_t>(rc);
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; x < rc;
+       x += stride) {
+    uint32_t id = static_cast<uint32_t>(x);
     const uint32_t r = static_cast<uint32_t>(x / p.C);
     const uint32_t j = static_cast<uint32_t>(x - static_cast<int64_t>(r) * p.C);
-    b = fast_mod(add_mod_p(rk[r], chunk_step(p.a, j)), p.fm_c, p.M);
+    uint32_t b = fast_mod(add_mod_p(rk[r], chunk_step(p.a, j)), p.fm_c, p.M);
     if (p.sign_mode) {
       const uint32_t h2 = add_mod_p(sign_hash0(rk[r], p.s_alpha, p.s_beta), chunk_step(p.a2, j));
       const uint32_t code = sign_code(h2, p.sign_mode);
       if (code == 2u) b = 0xffffffffu;
       id |= code << 31;  // code 1: negative (code 2 records are never read)
     }
+    cb[x] = b;
+    cv[x] = id;
   }
-  cb[x] = b;
-  cv[x] = id;
 }
 
 // info[0] = number of chunk records RC that read something (the sorted
 // records before the first sentinel), info[1] = records whose span wraps
-// (base > M - Z; a suffix of those RC).
+// (base > M - Z; a suffix of those RC), info[3] = RC + info[1].
 __global__ void tail_count_kernel(const KParams p, const uint32_t* __restrict__ cb,
                                   const uint32_t* __restrict__ num_runs, uint32_t* __restrict__ info) {
   uint64_t rc = static_cast<uint64_t>(*num_runs) * p.C;
@@ -235,6 +260,7 @@ __global__ void tail_count_kernel(const KParams p, const uint32_t* __restrict__ 
   }
   info[0] = static_cast<uint32_t>(rc);
   info[1] = static_cast<uint32_t>(rc - lo);
+  info[3] = static_cast<uint32_t>(rc + (rc - lo));  // length of the extended order
 }
 
 struct ExtList {  // the extended order: wrapped copies first, then all records
@@ -253,15 +279,15 @@ struct ExtList {  // the extended order: wrapped copies first, then all records
 __global__ __launch_bounds__(kBlockThreads) void own_kernel(const KParams p,
                                                             const uint32_t* __restrict__ cb,
                                                             const uint32_t* __restrict__ info,
-                                                            const int64_t cap2,
                                                             uint32_t* __restrict__ own) {
-  const int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
-  if (x >= cap2) return;
   ExtList e{cb, info[0], info[1], p.M};
-  uint32_t o = 0;
-  if (x < e.len()) {
+  const int64_t len = e.len();
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; x < len;
+       x += stride) {
+    uint32_t o = 0;
     const int64_t b = e.base(static_cast<uint32_t>(x));
-    const int64_t bn = x + 1 < e.len() ? e.base(static_cast<uint32_t>(x + 1)) : INT64_MAX;
+    const int64_t bn = x + 1 < len ? e.base(static_cast<uint32_t>(x + 1)) : INT64_MAX;
     if (bn != b) {  // last record of its base owns the elements
       const int64_t lo = b < 0 ? 0 : b;
       int64_t hi = b + p.Z;
@@ -269,44 +295,201 @@ __global__ __launch_bounds__(kBlockThreads) void own_kernel(const KParams p,
       if (hi > static_cast<int64_t>(p.M)) hi = p.M;
       o = hi > lo ? static_cast<uint32_t>(hi - lo) : 0u;
     }
+    own[x] = o;
   }
-  own[x] = o;
 }
 
+// Emit, element-parallel with balanced work.  A wavefront takes 64
+// consecutive records of the extended order; lane l holds record x = x0 + l,
+// the number of elements it owns o(x) (from the scanned ownership) and their
+// first output slot.  The wave expands its owned elements 64 at a time: the
+// lane for element e finds its record by a search over the lanes' prefix
+// sums, then sums, from the owner backwards, the run-sum entries of every
+// record covering its element (records are in base order, so the covering
+// ones are contiguous and end at the owner).  Sums run in a fixed order.
+// MODE 0 writes (location, value) at the element's output slot; MODE 1
+// applies SGD / Adagrad to the element in place (each element is owned once).
+struct EmitList {
+  uint32_t* locations;
+  float* values;
+  int64_t capacity;
+};
+template <typename WT>
+struct EmitUpdate {
+  WT* w;
+  float* s;
+  float lr, eps;
+};
+
+template <typename WT, bool ADAGRAD>
+__device__ __forceinline__ void update_element(const EmitUpdate<WT>& u, uint32_t m, float g) {
+  if (g == 0.f) return;  // untouched in value: keep the exact bits
+  float upd;
+  if (ADAGRAD) {
+    const float sn = u.s[m] + g * g;
+    u.s[m] = sn;
+    upd = u.lr * g / (sqrtf(sn) + u.eps);
+  } else {
+    upd = u.lr * g;
+  }
+  if constexpr (sizeof(WT) == 4) {
+    u.w[m] = u.w[m] - upd;
+  } else {
+    u.w[m] = f32_to_bf16_rne(bf16_to_f32(u.w[m]) - upd);
+  }
+}
+
+constexpr int kWalk = 4;     // covering records summed per round of a walk
+constexpr int kStage = 384;  // records a wavefront stages in LDS
+
+// Sum, for element m, of the run-sum entries of the records covering it,
+// walking from record `y0` backwards in walk order.  Rec(y) gives
+// (base, id | sign) of record y; the walk stops at the first record whose
+// span ends at or before m, or below record `ylo`.
+template <typename Rec>
+__device__ __forceinline__ float walk_sum(const KParams& p, const float* __restrict__ rs, int64_t m,
+                                          int64_t y0, int64_t ylo, Rec rec_of) {
+  const int64_t Z = p.Z;
+  float v = 0.f;
+  for (int64_t y = y0; y >= ylo; y -= kWalk) {
+    int64_t by[kWalk];
+    uint32_t rec[kWalk];
+    bool ok[kWalk];
+#pragma unroll
+    for (int u = 0; u < kWalk; ++u) {
+      ok[u] = y - u >= ylo;
+      by[u] = 0;
+      rec[u] = 0;
+      if (ok[u]) rec_of(y - u, by[u], rec[u]);
+      ok[u] = ok[u] && by[u] + Z > m;
+    }
+    float xv[kWalk];
+#pragma unroll
+    for (int u = 0; u < kWalk; ++u) {
+      const uint32_t id = rec[u] & 0x7fffffffu;
+      const uint32_t run = id / p.C, j = id - run * p.C;
+      xv[u] = ok[u] ? rs[static_cast<uint64_t>(run) * p.d + j * p.Z +
+                         static_cast<uint32_t>(m - by[u])]
+                    : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kWalk; ++u)
+      if (ok[u]) v += (rec[u] >> 31) ? -xv[u] : xv[u];
+    if (!ok[kWalk - 1]) break;
+  }
+  return v;
+}
+
+template <int MODE, typename WT, bool ADAGRAD>
 __global__ __launch_bounds__(kBlockThreads) void emit_kernel(
     const KParams p, const uint32_t* __restrict__ cb, const uint32_t* __restrict__ cv,
     const uint32_t* __restrict__ info, const uint32_t* __restrict__ slot,
-    const float* __restrict__ rs, const int64_t cap2, const int64_t capacity,
-    uint32_t* __restrict__ locations, float* __restrict__ values) {
-  const int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
-  if (x >= cap2) return;
-  ExtList e{cb, info[0], info[1], p.M};
-  if (x >= e.len()) return;
-  const int64_t b = e.base(static_cast<uint32_t>(x));
-  const int64_t bn = x + 1 < e.len() ? e.base(static_cast<uint32_t>(x + 1)) : INT64_MAX;
-  if (bn == b) return;
-  const int64_t lo = b < 0 ? 0 : b;
-  int64_t hi = b + p.Z;
-  if (bn < hi) hi = bn;
-  if (hi > static_cast<int64_t>(p.M)) hi = p.M;
-  uint64_t out = slot[x];
-  for (int64_t m = lo; m < hi; ++m, ++out) {
-    float v = 0.f;
-    // every record covering m sits at or before x in the extended order
-    for (int64_t y = x; y >= 0; --y) {
-      const int64_t by = e.base(static_cast<uint32_t>(y));
-      if (by + p.Z <= m) break;
-      const uint32_t rec = cv[e.sorted_index(static_cast<uint32_t>(y))];
-      const uint32_t id = rec & 0x7fffffffu;
-      const uint32_t run = id / p.C, j = id - run * p.C;
-      const float x = rs[static_cast<uint64_t>(run) * p.d + j * p.Z + static_cast<uint32_t>(m - by)];
-      v += (rec >> 31) ? -x : x;
+    const uint32_t* __restrict__ total, const float* __restrict__ rs, const EmitList list,
+    const EmitUpdate<WT> upd) {
+  __shared__ int32_t sbase_all[kWavesPerBlock][kStage];
+  __shared__ uint32_t srec_all[kWavesPerBlock][kStage];
+  int32_t* sbase = sbase_all[threadIdx.x >> 6];
+  uint32_t* srec = srec_all[threadIdx.x >> 6];
+  const int lane = threadIdx.x & (kWave - 1);
+  const ExtList el{cb, info[0], info[1], p.M};
+  const int64_t L = el.len();
+  const uint32_t U = *total;
+  const int64_t chunks = (L + kWave - 1) / kWave;
+  const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+  const int64_t Z = p.Z;
+  for (int64_t chunk = wave0; chunk < chunks; chunk += nwaves) {
+    const int64_t x0 = chunk * kWave;
+    const int64_t x = x0 + lane;
+    uint32_t o = 0, first = 0;
+    int64_t lo = 0;
+    if (x < L) {
+      first = slot[x];
+      o = (x + 1 < L ? slot[x + 1] : U) - first;
+      const int64_t b = el.base(static_cast<uint32_t>(x));
+      lo = b < 0 ? 0 : b;
     }
-    if (static_cast<int64_t>(out) < capacity) {
-      locations[out] = static_cast<uint32_t>(m);
-      values[out] = v;
+    // exclusive prefix of o over the lanes
+    uint32_t incl = o;
+#pragma unroll
+    for (int sh = 1; sh < kWave; sh <<= 1) {
+      const uint32_t y = __shfl_up(incl, sh);
+      if (lane >= sh) incl += y;
+    }
+    const uint32_t pre = incl - o;
+    const uint32_t T = __shfl(incl, kWave - 1);
+    if (T == 0) continue;
+    // Records before x0 that can still cover an element owned here: every
+    // such element is >= base(x0), so they are those with base > base(x0) - Z
+    // (a contiguous run ending at x0 - 1, bases being in ascending order).
+    const int64_t b0 = el.base(static_cast<uint32_t>(x0));
+    const int64_t xend = x0 + kWave < L ? x0 + kWave : L;
+    int64_t ymin = x0;
+    bool fits = true;
+    while (ymin > 0) {
+      const int64_t y = ymin - 1 - lane;
+      const bool cov = y >= 0 && el.base(static_cast<uint32_t>(y)) + Z > b0;
+      const uint64_t stop = __ballot(!cov);
+      if (stop == 0) {  // all 64 records before ymin cover: keep going back
+        ymin -= kWave;
+        if (xend - ymin > kStage) {  // too many to stage: walk from memory
+          fits = false;
+          break;
+        }
+        continue;
+      }
+      ymin -= __builtin_ctzll(stop);
+      break;
+    }
+    const bool staged = fits && xend - ymin <= kStage;
+    if (staged) {
+      // the previous chunk's reads of this wave's LDS rows are complete
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      for (int64_t i = lane; i < xend - ymin; i += kWave) {
+        sbase[i] = static_cast<int32_t>(el.base(static_cast<uint32_t>(ymin + i)));
+        srec[i] = cv[el.sorted_index(static_cast<uint32_t>(ymin + i))];
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+    }
+    for (uint32_t b0e = 0; b0e < T; b0e += kWave) {
+      const uint32_t e = b0e + static_cast<uint32_t>(lane);
+      // record of element e: the largest lane r with pre[r] <= e
+      int r = 0;
+#pragma unroll
+      for (int step = kWave / 2; step >= 1; step >>= 1) {
+        const int probe = r + step;
+        if (__shfl(pre, probe) <= e) r = probe;
+      }
+      const uint32_t off = e - __shfl(pre, r);
+      const int64_t xr = x0 + r;
+      const int64_t m = __shfl(lo, r) + off;
+      const uint32_t k = __shfl(first, r) + off;
+      if (e >= T) continue;
+      float v;
+      if (staged) {
+        v = walk_sum(p, rs, m, xr - ymin, 0, [&](int64_t y, int64_t& by, uint32_t& rec) {
+          by = sbase[y];
+          rec = srec[y];
+        });
+      } else {
+        v = walk_sum(p, rs, m, xr, 0, [&](int64_t y, int64_t& by, uint32_t& rec) {
+          by = el.base(static_cast<uint32_t>(y));
+          rec = cv[el.sorted_index(static_cast<uint32_t>(y))];
+        });
+      }
+      if (MODE == 0) {
+        if (static_cast<int64_t>(k) < list.capacity) {
+          list.locations[k] = static_cast<uint32_t>(m);
+          list.values[k] = v;
+        }
+      } else {
+        update_element<WT, ADAGRAD>(upd, static_cast<uint32_t>(m), v);
+      }
     }
   }
+  (void)Z;
 }
 
 __global__ void store_count_kernel(const uint32_t* __restrict__ total, int64_t* __restrict__ out) {
@@ -368,14 +551,29 @@ static void launch_run_sums(const KParams& p, const uint32_t* keys, const uint32
   else launch_run_sums_t<8, 2>(p, keys, rows, run_off, grad, inv_len, rs, rk, stream);
 }
 
-static uint32_t blocks_for(int64_t n) {
-  return static_cast<uint32_t>((n + kBlockThreads - 1) / kBlockThreads);
+// Blocks of a grid-stride launch over at most n items.
+static uint32_t grid_stride_blocks(int64_t n) {
+  const int64_t b = (n + kBlockThreads - 1) / kBlockThreads;
+  return static_cast<uint32_t>(b < 1 ? 1 : (b > 8192 ? 8192 : b));
 }
 
-hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const void* offsets,
-                                  const void* grad, void* workspace, uint32_t* locations,
-                                  float* values, int64_t capacity, uint32_t* num_unique32,
-                                  hipStream_t stream) {
+static uint32_t emit_blocks(int64_t cap2) {
+  const int64_t waves = (cap2 + kWave - 1) / kWave;
+  const int64_t want = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+  return static_cast<uint32_t>(want < 1 ? 1 : (want > 16384 ? 16384 : want));
+}
+
+// Everything up to the scanned ownership; returns the buffers the emit
+// step reads.
+struct SparseState {
+  const uint32_t *cb, *cv, *info, *own;
+  const float* rs;
+  int64_t cap2;
+};
+
+static hipError_t sparse_prepare(const KParams& p, const void* indices, const void* offsets,
+                                 const void* grad, void* workspace, uint32_t* num_unique32,
+                                 SparseState* st, hipStream_t stream) {
   const int64_t N = p.N, cap = record_cap(p), cap2 = 2 * cap;
   const int64_t npieces = (N + kWave - 1) / kWave;
   char* cur = static_cast<char*>(workspace);
@@ -410,76 +608,65 @@ hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const v
     launch_run_sums(p, k0, v0, runs, static_cast<const uint16_t*>(grad), inv_len, rs, rk, stream);
   else
     launch_run_sums(p, k0, v0, runs, static_cast<const float*>(grad), inv_len, rs, rk, stream);
-  hipLaunchKernelGGL(chunk_records_kernel, dim3(blocks_for(cap)), dim3(kBlockThreads), 0, stream, p,
-                     rk, num_runs, cap, cb, cv);
+  hipLaunchKernelGGL(chunk_records_kernel, dim3(grid_stride_blocks(cap)), dim3(kBlockThreads), 0,
+                     stream, p, rk, num_runs, cap, cb, cv, info);
   e = hipGetLastError();
-  if (e == hipSuccess) e = radix_sort_pairs(cb, cv, cb1, cv1, cap, base_bits(p.M), cscr, stream);
+  uint32_t* cbs = cb;
+  uint32_t* cvs = cv;
+  // only the runs * C records that exist are sorted, owned and scanned
+  if (e == hipSuccess)
+    e = radix_sort_pairs(cbs, cvs, cb1, cv1, cap, base_bits(p.M), cscr, stream, info + 2);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(tail_count_kernel, dim3(1), dim3(1), 0, stream, p, cb, num_runs, info);
-  hipLaunchKernelGGL(own_kernel, dim3(blocks_for(cap2)), dim3(kBlockThreads), 0, stream, p, cb, info,
-                     cap2, own);
-  e = exclusive_scan(own, cap2, oscr, num_unique32, stream);
+  hipLaunchKernelGGL(tail_count_kernel, dim3(1), dim3(1), 0, stream, p, cbs, num_runs, info);
+  hipLaunchKernelGGL(own_kernel, dim3(grid_stride_blocks(cap2)), dim3(kBlockThreads), 0, stream, p,
+                     cbs, info, own);
+  e = exclusive_scan(own, cap2, oscr, num_unique32, stream, info + 3);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(emit_kernel, dim3(blocks_for(cap2)), dim3(kBlockThreads), 0, stream, p, cb, cv,
-                     info, own, rs, cap2, capacity, locations, values);
+  *st = SparseState{cbs, cvs, info, own, rs, cap2};
+  return hipSuccess;
+}
+
+hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const void* offsets,
+                                  const void* grad, void* workspace, uint32_t* locations,
+                                  float* values, int64_t capacity, uint32_t* num_unique32,
+                                  hipStream_t stream) {
+  SparseState st;
+  hipError_t e = sparse_prepare(p, indices, offsets, grad, workspace, num_unique32, &st, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((emit_kernel<0, float, false>), dim3(emit_blocks(st.cap2)), dim3(kBlockThreads),
+                     0, stream, p, st.cb, st.cv, st.info, st.own, num_unique32, st.rs,
+                     EmitList{locations, values, capacity}, EmitUpdate<float>{nullptr, nullptr, 0.f, 0.f});
+  return hipGetLastError();
+}
+
+template <typename WT>
+static void launch_emit_update(const KParams& p, const SparseState& st, const uint32_t* total,
+                               WT* w, float* state, float lr, float eps, hipStream_t stream) {
+  const EmitList none{nullptr, nullptr, 0};
+  const EmitUpdate<WT> u{w, state, lr, eps};
+  if (state)
+    hipLaunchKernelGGL((emit_kernel<1, WT, true>), dim3(emit_blocks(st.cap2)), dim3(kBlockThreads), 0,
+                       stream, p, st.cb, st.cv, st.info, st.own, total, st.rs, none, u);
+  else
+    hipLaunchKernelGGL((emit_kernel<1, WT, false>), dim3(emit_blocks(st.cap2)), dim3(kBlockThreads), 0,
+                       stream, p, st.cb, st.cv, st.info, st.own, total, st.rs, none, u);
+}
+
+hipError_t launch_sparse_update(const KParams& p, const void* indices, const void* offsets,
+                                const void* grad, void* workspace, uint32_t* num_unique32, void* w,
+                                bool bf16, float* state, float lr, float eps, hipStream_t stream) {
+  SparseState st;
+  hipError_t e = sparse_prepare(p, indices, offsets, grad, workspace, num_unique32, &st, stream);
+  if (e != hipSuccess) return e;
+  if (bf16)
+    launch_emit_update(p, st, num_unique32, static_cast<uint16_t*>(w), state, lr, eps, stream);
+  else
+    launch_emit_update(p, st, num_unique32, static_cast<float*>(w), state, lr, eps, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_store_count(const uint32_t* total, int64_t* out, hipStream_t stream) {
   hipLaunchKernelGGL(store_count_kernel, dim3(1), dim3(1), 0, stream, total, out);
-  return hipGetLastError();
-}
-
-// Optimizer on the unique locations only (no two entries share a location).
-template <typename WT, bool ADAGRAD>
-__global__ __launch_bounds__(kBlockThreads) void sparse_optimizer_kernel(
-    WT* __restrict__ w, float* __restrict__ s, const uint32_t* __restrict__ loc,
-    const float* __restrict__ val, const uint32_t* __restrict__ count, const int64_t capacity,
-    const float lr, const float eps) {
-  const int64_t n = *count < capacity ? static_cast<int64_t>(*count) : capacity;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
-  for (int64_t k = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; k < n; k += stride) {
-    const uint32_t m = loc[k];
-    const float g = val[k];
-    if (g == 0.f) continue;
-    float upd;
-    if (ADAGRAD) {
-      const float sn = s[m] + g * g;
-      s[m] = sn;
-      upd = lr * g / (sqrtf(sn) + eps);
-    } else {
-      upd = lr * g;
-    }
-    if constexpr (sizeof(WT) == 4) {
-      w[m] = w[m] - upd;
-    } else {
-      w[m] = f32_to_bf16_rne(bf16_to_f32(w[m]) - upd);
-    }
-  }
-}
-
-hipError_t launch_sparse_optimizer(void* w, bool bf16, float* state, const uint32_t* loc,
-                                   const float* val, const uint32_t* count, int64_t capacity,
-                                   float lr, float eps, hipStream_t stream) {
-  const int64_t want = (capacity + kBlockThreads * 4 - 1) / (kBlockThreads * 4);
-  const dim3 grid(static_cast<uint32_t>(want < 1 ? 1 : (want > 8192 ? 8192 : want)));
-  if (bf16) {
-    uint16_t* wb = static_cast<uint16_t*>(w);
-    if (state)
-      hipLaunchKernelGGL((sparse_optimizer_kernel<uint16_t, true>), grid, dim3(kBlockThreads), 0, stream,
-                         wb, state, loc, val, count, capacity, lr, eps);
-    else
-      hipLaunchKernelGGL((sparse_optimizer_kernel<uint16_t, false>), grid, dim3(kBlockThreads), 0, stream,
-                         wb, state, loc, val, count, capacity, lr, eps);
-  } else {
-    float* wf = static_cast<float*>(w);
-    if (state)
-      hipLaunchKernelGGL((sparse_optimizer_kernel<float, true>), grid, dim3(kBlockThreads), 0, stream, wf,
-                         state, loc, val, count, capacity, lr, eps);
-    else
-      hipLaunchKernelGGL((sparse_optimizer_kernel<float, false>), grid, dim3(kBlockThreads), 0, stream, wf,
-                         state, loc, val, count, capacity, lr, eps);
-  }
   return hipGetLastError();
 }
 

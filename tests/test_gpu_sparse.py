@@ -19,7 +19,12 @@ CASES = [("c1", None, {}), ("c2", 700, {}), ("c3", 50, {}), ("c4", 300, dict(M=5
          ("c5", 900, {}),
          ("wrap-z3-m61", 33, dict(d=24, Z=3, M=61)), ("z-equals-m", 40, dict(d=32, Z=32, M=32)),
          ("m-one", 40, dict(d=4, Z=1, M=1)), ("empty-and-long", 70, dict(bag="poisson:30:0:200")),
-         ("d640", 20, dict(d=640, Z=64))]
+         ("d640", 20, dict(d=640, Z=64)),
+         # thousands of chunk records over 100 elements: the records covering
+         # a wavefront's elements exceed what it stages, so the merge walks
+         # them from memory
+         ("heavy-coverage", 300, dict(d=64, Z=16, M=100, bag="poisson:8:0:30")),
+         ("medium-coverage", 300, dict(d=64, Z=16, M=3000, bag="poisson:8:0:30"))]
 
 
 def _wl(key, over):
@@ -81,3 +86,18 @@ def test_sparse_update_is_deterministic():
         L.backward(synth.make_grad(wl, B=200))
         outs.append((L.weights().view(np.uint32).copy(), L.state.cpu().numpy().view(np.uint32)))
     assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+
+
+@pytest.mark.parametrize("opt", ["sgd", "adagrad"])
+@pytest.mark.parametrize("M", [100, 3000])
+def test_sparse_update_heavy_coverage(opt, M):
+    """The SPARSE backward variant (update applied at each location as it is
+    summed) when many chunk records cover each element."""
+    import parity
+    wl = synth.get("c1").scaled(d=64, Z=16, M=M, bag="poisson:8:0:30", optimizer=opt, lr=0.05)
+    L = Layer(wl, B=300, flags=pss.PSS_BWD_SPARSE)
+    g = synth.make_grad(wl, B=L.B)
+    L.backward(g)
+    w_ref, s_ref, G, A, _ = L.ref_backward(g)
+    s_gpu = None if L.state is None else L.state.cpu().numpy()
+    parity.check_update(L, L.weights(), s_gpu, w_ref, s_ref, G, A, wl.lr)

@@ -35,15 +35,23 @@ ROTATE = 4
 PMC_FILE = os.path.join(ROOT, "profiles", "pmc_forward_c2.json")
 
 
-def source_digest() -> str:
-    """sha256 over the HIP sources of the library (kernels and headers)."""
+# Sources each profiled kernel is compiled from (its own file and the shared
+# device headers): a counter summary stays valid while these are unchanged.
+KERNEL_SOURCES = {
+    "forward_kernel": ["pss_forward.hip"],
+    "reduce_deposit_kernel": ["pss_sorted.hip"],
+}
+SHARED_HEADERS = ["pss_hash.hpp", "pss_kernels.hpp"]  # device code; pss_launch.hpp only declares
+
+
+def source_digest(kernel: str = "forward_kernel") -> str:
+    """sha256 over the HIP sources a kernel is built from."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2207_10731_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in sorted(KERNEL_SOURCES[kernel] + SHARED_HEADERS):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 
@@ -55,7 +63,7 @@ def counted_traffic(workload: str):
             pmc = json.load(f)
     except (OSError, ValueError):
         return None
-    if pmc.get("source_sha256") != source_digest() or pmc.get("workload") != workload:
+    if pmc.get("source_sha256") != source_digest("forward_kernel") or pmc.get("workload") != workload:
         return None
     return pmc["fetch_kib"] * 1024 * pmc["fetch_scale"] + pmc["write_kib"] * 1024 * pmc["write_scale"]
 

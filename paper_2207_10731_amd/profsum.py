@@ -7,8 +7,9 @@
       --fetch F.db --write W.db --copy-fetch CF.db --copy-write CW.db \\
       --copy-bytes BYTES --out profiles/pmc_<kernel>_<workload>.json
       FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the kernel whose name
-      contains SUBSTR, with scale factors from a copy kernel that moved
-      BYTES each way, and the sha256 of the library sources they were taken on
+      contains SUBSTR (forward_kernel or reduce_deposit_kernel), with scale
+      factors from a copy kernel that moved BYTES each way, and the sha256 of
+      the sources that kernel is built from
 """
 from __future__ import annotations
 
@@ -71,7 +72,8 @@ def main(argv=None):
         "copy_fetch_kib": cfetch,
         "copy_write_kib": cwrite,
         "copy_bytes": a.copy_bytes,
-        "source_sha256": bench.source_digest(),
+        "source_sha256": bench.source_digest(a.kernel),
+        "source_files": sorted(bench.KERNEL_SOURCES[a.kernel] + bench.SHARED_HEADERS),
         "command": a.command,
     }
     rec["hbm_bytes_per_dispatch"] = (rec["fetch_kib"] * 1024 * rec["fetch_scale"]

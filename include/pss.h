@@ -86,7 +86,9 @@ enum {
 };
 
 /* Backward variant, bits 0-1 of pss_hash_params.flags.
- *   AUTO    library's choice for the shape (currently SORTED).
+ *   AUTO    library's choice for the shape: SPARSE when the update is not
+ *           fused (Adagrad, or bfloat16 storage) and M > 16 * N * d (low
+ *           compression: a pass over all of M would dominate), else SORTED.
  *   ATOMIC  every (lookup, dim) contribution added with a float atomic, into
  *           `shared` (SGD on float32 storage) or into a float32 gradient
  *           buffer followed by one streaming optimizer pass.

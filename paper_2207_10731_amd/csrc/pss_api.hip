@@ -89,6 +89,19 @@ int64_t sparse_capacity(int64_t M, const KParams& p) {
   return nd < M ? nd : M;
 }
 
+// AUTO's choice (paper Sec. 3: dense gradients win at high compression,
+// sparse ones cost the same at any compression).  A fused SGD update costs
+// nothing per element of M, so SORTED.  An unfused update (Adagrad, bf16
+// storage) pays a pass over all M elements; when M exceeds 16 times the
+// batch's N*d reads (low compression) the sparse path, whose cost follows
+// the batch, is cheaper: measured crossover between 10x and 100x compression
+// at batch 10240, d = 128.
+uint32_t auto_variant(int64_t M, const KParams& p, bool unfused, bool sparse_fits) {
+  const int64_t reads = p.N * static_cast<int64_t>(p.d);
+  if (unfused && sparse_fits && M > 16 * reads) return PSS_BWD_SPARSE;
+  return PSS_BWD_SORTED;
+}
+
 hipError_t pool_for_current_device(hipMemPool_t* out) {
   int dev = 0;
   hipError_t st = hipGetDevice(&dev);
@@ -174,12 +187,13 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (!isfinite(lr)) return PSS_ERR_INVALID_ARG;
   if (state != nullptr && !(hash_params->eps >= 0.f && isfinite(hash_params->eps)))
     return PSS_ERR_INVALID_ARG;
-  const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
+  uint32_t variant = hash_params->flags & PSS_BWD_MASK;
   const KParams p = make_params(M, Z, d, hash_params);
   const bool bf16 = hash_params->weight_dtype == PSS_BF16;
-  if (variant == PSS_BWD_SPARSE && p.N * static_cast<int64_t>(p.C) >= (1ll << 31))
-    return PSS_ERR_UNSUPPORTED;
+  const bool sparse_fits = p.N * static_cast<int64_t>(p.C) < (1ll << 31);
+  if (variant == PSS_BWD_SPARSE && !sparse_fits) return PSS_ERR_UNSUPPORTED;
   if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
+  if (variant == PSS_BWD_AUTO) variant = auto_variant(M, p, state != nullptr || bf16, sparse_fits);
 
   if (variant == PSS_BWD_SPARSE) {
     // Alg. 1 sparse branch: unique locations + summed values, with the

@@ -14,12 +14,13 @@
 //             per pass a histogram kernel, a per-digit scan (one workgroup
 //             per digit) and a scatter kernel whose per-wave ranks come from
 //             ballot matching (no atomics on the data path).
-//   reduce    one wavefront per 64 consecutive sorted pairs: sort them by
-//             the full h0 (bitonic network over the lanes), accumulate the
-//             gradient rows of each run of equal h0 in registers (lanes over
-//             the dims), then add the run's sum at the run's hashed
-//             addresses with float atomics.  A token spanning several
-//             wavefronts deposits one partial sum per wavefront.
+//   reduce    one workgroup per 256 consecutive sorted pairs: sort them by
+//             the full h0 (bitonic network per wavefront, then a merge of
+//             the four lists through LDS), accumulate the gradient rows of
+//             each run of equal h0 in registers (lanes over the dims), then
+//             add the run's sum at the run's hashed addresses with float
+//             atomics.  A token spanning several pieces deposits one partial
+//             sum per piece.
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -220,90 +221,227 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
 // ---------------------------------------------------------------------------
 // segmented reduction + deposit
 // ---------------------------------------------------------------------------
-template <int EPL, int U, bool TAB, bool SIGN, typename GT>
-__global__ __launch_bounds__(kBlockThreads) void reduce_deposit_kernel(
+// One workgroup per piece of kPiece = 256 consecutive pairs of the grouped
+// order, with two kinds of wavefronts:
+//
+//  * 4 readers.  Each sorts 64 pairs by the full key in registers (bitonic);
+//    the four sorted lists are merged through LDS (a pair's rank is its own
+//    index plus, per other list, how many of that list's pairs precede it: a
+//    7-step binary search), so every token of the piece forms one run.  A
+//    reader then walks its quarter of the merged order U rows at a time,
+//    sums the gradient rows of each run in registers (lanes over the dims)
+//    and hands every finished run sum to its depositor through LDS.
+//  * 4 depositors.  Each adds the run sums of its reader at the runs' hashed
+//    addresses with float atomics.
+//
+// Why two kinds: on gfx9 loads and atomics count in one in-order wait
+// counter, so a wavefront that did both would wait for its last batch's
+// atomics (which resolve far away, at the memory side) before it could use
+// its next batch's rows.  Split, the readers' waits cover loads only and the
+// depositors never wait for memory at all.  Readers and depositors step in
+// phases separated by workgroup barriers (LDS-only fences: no wait for the
+// atomics); in phase k a reader fills buffer k mod 2 while its depositor
+// drains buffer (k-1) mod 2.  Rows of batch k+1 are requested before batch
+// k is summed.  A run crossing a quarter boundary deposits once per quarter.
+constexpr int kPiece = 256;                 // pairs per workgroup
+constexpr int kReaders = kPiece / kWave;    // 4
+constexpr int kReduceThreads = 2 * kPiece;  // readers + depositors
+constexpr int kSlotFloats = 1024;           // per buffer: U run sums of 64 * EPL dims
+
+// How many of the 64 sorted keys in `list` precede `key`: all smaller keys,
+// and equal keys too when `ties` (the list comes earlier in merge order).
+__device__ __forceinline__ int count_before(const uint32_t* list, uint32_t key, bool ties) {
+  int c = 0;
+#pragma unroll
+  for (int step = kWave; step >= 1; step >>= 1) {
+    if (c + step <= kWave) {
+      const uint32_t k = list[c + step - 1];
+      if (k < key || (ties && k == key)) c += step;
+    }
+  }
+  return c;
+}
+
+// Workgroup barrier whose fences cover LDS only: global atomics in flight
+// are not waited for.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Rows of U merged positions (q .. q+U-1 of the quarter, clamped to its last
+// position) into g; lanes over the dims, mean pooling applied.
+template <int EPL, int U, typename GT>
+__device__ __forceinline__ void load_rows(float (&g)[U][EPL], const GT* __restrict__ grad,
+                                          const float* __restrict__ inv_len, const KParams& p,
+                                          uint32_t wr, int q, int nq, uint32_t c0, int lane,
+                                          const bool* act) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int uu = q + u < nq ? q + u : nq - 1;
+    const uint32_t ru = readlane_u32(wr, uu);
+    const GT* grow = grad + static_cast<uint64_t>(ru) * p.d;
+    const float il = p.mean ? inv_len[ru] : 1.f;
+#pragma unroll
+    for (int r = 0; r < EPL; ++r) {
+      const float x = load_row(grow, act[r] ? c0 + lane + kWave * r : 0u);
+      g[u][r] = p.mean ? x * il : x;
+    }
+  }
+}
+
+// Sums the rows of positions q .. q+U-1 into acc; every run that ends there
+// goes to the buffer (values, key); returns the number of runs written.
+template <int EPL, int U>
+__device__ __forceinline__ int sum_runs(const float (&g)[U][EPL], float* acc, uint32_t wk, int q,
+                                        int nq, uint32_t after, float* vals, uint32_t* rkeys,
+                                        int lane) {
+  int nrun = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    if (q + u < nq) {
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) acc[r] += g[u][r];
+      const uint32_t h = readlane_u32(wk, q + u);
+      const uint32_t hn = q + u + 1 < nq ? readlane_u32(wk, q + u + 1) : after;
+      if (hn != h) {
+#pragma unroll
+        for (int r = 0; r < EPL; ++r) {
+          vals[nrun * (kWave * EPL) + kWave * r + lane] = acc[r];
+          acc[r] = 0.f;
+        }
+        if (lane == 0) rkeys[nrun] = h;
+        ++nrun;
+      }
+    }
+  }
+  return nrun;
+}
+
+template <int EPL, int U, bool SIGN, typename GT>
+__global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
     float* __restrict__ dst, const float scale, const KParams p,
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ rows,
     const GT* __restrict__ grad, const float* __restrict__ inv_len, const int64_t n) {
+  static_assert(U * kWave * EPL == kSlotFloats, "a buffer holds U run sums");
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t p0 = (static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6)) * kWave;
-  if (p0 >= n) return;
-  const int cnt = n - p0 < kWave ? static_cast<int>(n - p0) : kWave;
+  const int w = static_cast<int>(__builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
+  const bool reader = w < kReaders;
+  const int pair = reader ? w : w - kReaders;
+  const int64_t p0 = static_cast<int64_t>(blockIdx.x) * kPiece;
+  if (p0 >= n) return;  // whole workgroup
+  const int cnt = n - p0 < kPiece ? static_cast<int>(n - p0) : kPiece;
   const uint32_t c0 = blockIdx.y * (kWave * EPL);
-  __shared__ uint32_t tab_all[TAB ? kWavesPerBlock * kWave * kTabStride : 1];
-  uint32_t* tab = tab_all + (TAB ? (threadIdx.x >> 6) * kWave * kTabStride : 0);
+  __shared__ uint32_t lk[kPiece], lr[kPiece];  // the readers' sorted lists
+  __shared__ uint32_t mk[kPiece], mr[kPiece];  // merged order
+  __shared__ float vals[kReaders][2][kSlotFloats];
+  __shared__ uint32_t rkeys[kReaders][2][U];
+  __shared__ int nruns[kReaders][2];
 
-  uint32_t step[EPL], step2[EPL], kk[EPL], jj[EPL];
   bool act[EPL];
 #pragma unroll
-  for (int r = 0; r < EPL; ++r) {
-    const uint32_t c = c0 + lane + kWave * r;
-    act[r] = c < p.d;
-    const uint32_t cc = act[r] ? c : 0;
-    jj[r] = cc / p.Z;
-    kk[r] = cc - jj[r] * p.Z;
-    step[r] = TAB ? 0u : chunk_step(p.a, jj[r]);
-    step2[r] = (TAB || !SIGN) ? 0u : chunk_step(p.a2, jj[r]);
-  }
-  uint32_t key = 0xffffffffu, row = 0;
-  if (lane < cnt) {
-    key = keys[p0 + lane];
-    row = rows[p0 + lane];
-    if (row >= p.num_bags) row = 0;  // rows come from keygen; clamp keeps reads in bounds
-  }
-  // Bitonic sort of the wave's 64 (key, row) pairs by the full key: the
-  // global sort only orders the low bits, so tokens that share them can
-  // arrive interleaved; sorted, each token of the piece forms one run.
-  // Empty lanes hold key 0xffffffff (> any hash) and stay at the end.
-  wave_sort_pairs(key, row, lane);
-  // lane l: chunk bases of the key it holds after the sort
-  if (TAB) fill_base_table<SIGN>(tab, key, p, lane);
-  float acc[EPL];
-#pragma unroll
-  for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
+  for (int r = 0; r < EPL; ++r) act[r] = c0 + lane + kWave * r < p.d;
 
-  for (int q = 0; q < cnt; q += U) {
-    // Load phase: straight-line, U rows in flight (past-the-end positions
-    // re-read the last row of the piece; inactive dims read the row start).
-    float gv[U][EPL];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int uu = q + u < cnt ? q + u : cnt - 1;
-      const uint32_t ru = readlane_u32(row, uu);
-      const GT* grow = grad + static_cast<uint64_t>(ru) * p.d;
-      const float il = p.mean ? inv_len[ru] : 1.f;
-#pragma unroll
-      for (int r = 0; r < EPL; ++r) {
-        const float x = load_row(grow, act[r] ? c0 + lane + kWave * r : 0u);
-        gv[u][r] = p.mean ? x * il : x;
-      }
+  // 1. readers sort their pairs; empty slots hold key 0xffffffff (above any
+  //    hash) and stay behind every real pair
+  const int my = pair * kWave + lane;
+  uint32_t key = 0xffffffffu, row = 0;
+  if (reader) {
+    if (my < cnt) {
+      key = keys[p0 + my];
+      row = rows[p0 + my];
+      if (row >= p.num_bags) row = 0;  // rows come from keygen; clamp keeps reads in bounds
     }
-    // Reduce phase: deposits (atomics) only after every load of the batch
-    // was issued; loads and atomics share one wait counter on gfx9.
+    wave_sort_pairs(key, row, lane);
+    lk[my] = key;
+    lr[my] = row;
+  }
+  lds_barrier();
+  // 2. merge: stable across lists (equal keys of an earlier list first)
+  if (reader) {
+    int rank = lane;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (q + u < cnt) {
+    for (int v = 0; v < kReaders; ++v)
+      if (v != w) rank += count_before(lk + v * kWave, key, v < w);
+    mk[rank] = key;
+    mr[rank] = row;
+  }
+  lds_barrier();
+
+  // 3. phases: reader sums batch k into buffer k&1, depositor drains the
+  //    other buffer.  Every wavefront runs the same number of phases.
+  const int q0 = pair * kWave;
+  const int nq = cnt - q0 < kWave ? (cnt - q0 > 0 ? cnt - q0 : 0) : kWave;
+  constexpr int kBatches = kWave / U;
+  if (reader && nq > 0) {
+    const uint32_t wk = mk[my];
+    const uint32_t wr = mr[my];
+    // key after the quarter: a run that continues into the next quarter is
+    // cut here (it deposits once per quarter)
+    const uint32_t after = 0xffffffffu;
+    float acc[EPL];
 #pragma unroll
-        for (int r = 0; r < EPL; ++r) acc[r] += gv[u][r];
-        const uint32_t h = readlane_u32(key, q + u);
-        const uint32_t hn = q + u + 1 < cnt ? readlane_u32(key, q + u + 1) : ~h;
-        if (hn != h) {
-          const uint32_t h20 = (!TAB && SIGN) ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
+    for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
+    float ga[U][EPL], gb[U][EPL];
+    load_rows<EPL, U>(ga, grad, inv_len, p, wr, 0, nq, c0, lane, act);
+#pragma unroll
+    for (int k = 0; k <= kBatches; ++k) {
+      if (k < kBatches) {
+        const int q = k * U;
+        // Rows of the next batch are requested before this one is summed
+        // (unconditionally, so that the wait for this batch's rows is exact;
+        // past the quarter's end they repeat its last row).
+        if (k + 1 < kBatches) {
+          if (k & 1) load_rows<EPL, U>(ga, grad, inv_len, p, wr, q + U, nq, c0, lane, act);
+          else load_rows<EPL, U>(gb, grad, inv_len, p, wr, q + U, nq, c0, lane, act);
+        }
+        int nr = 0;
+        if (q < nq)
+          nr = (k & 1) ? sum_runs<EPL, U>(gb, acc, wk, q, nq, after, vals[pair][k & 1],
+                                          rkeys[pair][k & 1], lane)
+                       : sum_runs<EPL, U>(ga, acc, wk, q, nq, after, vals[pair][k & 1],
+                                          rkeys[pair][k & 1], lane);
+        if (lane == 0) nruns[pair][k & 1] = nr;
+      }
+      lds_barrier();
+    }
+  } else if (reader) {  // an empty quarter (last piece): no runs
+#pragma unroll
+    for (int k = 0; k <= kBatches; ++k) {
+      if (k < kBatches && lane == 0) nruns[pair][k & 1] = 0;
+      lds_barrier();
+    }
+  } else {
+    uint32_t step[EPL], step2[EPL], kk[EPL];
+#pragma unroll
+    for (int r = 0; r < EPL; ++r) {
+      const uint32_t cc = act[r] ? c0 + lane + kWave * r : 0u;
+      const uint32_t jj = cc / p.Z;
+      kk[r] = cc - jj * p.Z;
+      step[r] = chunk_step(p.a, jj);
+      step2[r] = SIGN ? chunk_step(p.a2, jj) : 0u;
+    }
+#pragma unroll
+    for (int k = 0; k <= kBatches; ++k) {
+      if (k > 0) {
+        const int b = (k - 1) & 1;
+        const int nr = nruns[pair][b];
+        for (int s = 0; s < nr; ++s) {
+          const uint32_t h = rkeys[pair][b][s];
+          const uint32_t h20 = SIGN ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
 #pragma unroll
           for (int r = 0; r < EPL; ++r) {
-            if (act[r]) {
-              const uint32_t ent =
-                  TAB ? tab[(q + u) * kTabStride + jj[r]]
-                      : chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M),
-                                          add_mod_p(h20, step2[r]), p);
-              const Elem el = elem_of<SIGN>(ent, kk[r], p.M);
-              if (!SIGN || el.read)
-                unsafeAtomicAdd(dst + el.m, SIGN ? apply_sign(scale * acc[r], el) : scale * acc[r]);
-            }
-            acc[r] = 0.f;
+            if (!act[r]) continue;
+            const uint32_t ent = chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M),
+                                                   add_mod_p(h20, step2[r]), p);
+            const Elem el = elem_of<SIGN>(ent, kk[r], p.M);
+            const float v = scale * vals[pair][b][s * (kWave * EPL) + kWave * r + lane];
+            if (!SIGN || el.read) unsafeAtomicAdd(dst + el.m, SIGN ? apply_sign(v, el) : v);
           }
         }
       }
+      lds_barrier();
     }
   }
 }
@@ -364,36 +502,26 @@ hipError_t launch_keygen(const KParams& p, const void* indices, const void* offs
   return hipGetLastError();
 }
 
-template <int EPL, int U, bool TAB, bool SIGN, typename GT>
+template <int EPL, int U, bool SIGN, typename GT>
 static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const GT* grad, const float* inv_len,
                                   hipStream_t stream) {
-  const uint64_t waves = (static_cast<uint64_t>(p.N) + kWave - 1) / kWave;
-  const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+  const uint64_t blocks = (static_cast<uint64_t>(p.N) + kPiece - 1) / kPiece;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
-  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, TAB, SIGN, GT>),
-                     dim3(static_cast<uint32_t>(blocks), slabs), dim3(kBlockThreads), 0, stream, dst,
-                     scale, p, keys, rows, grad, inv_len, p.N);
+  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT>),
+                     dim3(static_cast<uint32_t>(blocks), slabs), dim3(kReduceThreads), 0, stream,
+                     dst, scale, p, keys, rows, grad, inv_len, p.N);
   return hipGetLastError();
-}
-
-template <bool TAB, bool SIGN, typename GT>
-static hipError_t launch_reduce_c(float* dst, float scale, const KParams& p, const uint32_t* keys,
-                                  const uint32_t* rows, const GT* grad, const float* il,
-                                  hipStream_t stream) {
-  if (p.d <= 64) return launch_reduce_t<1, 16, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  if (p.d <= 128) return launch_reduce_t<2, 8, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  if (p.d <= 256) return launch_reduce_t<4, 4, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  return launch_reduce_t<8, 2, TAB, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
 }
 
 template <bool SIGN, typename GT>
 static hipError_t launch_reduce_s(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const GT* grad, const float* il,
                                   hipStream_t stream) {
-  if (p.C <= static_cast<uint32_t>(kTabChunks))
-    return launch_reduce_c<true, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  return launch_reduce_c<false, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  if (p.d <= 64) return launch_reduce_t<1, 16, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  if (p.d <= 128) return launch_reduce_t<2, 8, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  if (p.d <= 256) return launch_reduce_t<4, 4, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+  return launch_reduce_t<8, 2, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
 }
 
 template <typename GT>

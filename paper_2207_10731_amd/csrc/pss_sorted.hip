@@ -52,6 +52,15 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_kernel(
   const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
   const uint32_t rr = b * p.T + t;
   if (p.mean && lane < tl.nb && tl.len) inv_len[rr] = 1.f / static_cast<float>(tl.len);
+  if (__ballot(lane >= tl.nb || tl.len == 1) == ~0ull) {
+    // one-hot tile: item E0 + l belongs to bag l
+    if (lane < tl.nb) {
+      const int64_t e = tl.E0 + lane;
+      keys[e] = item_hash(load_index(indices, e, p.idx32), tl.tC, p.TC, p.a, p.b);
+      rows[e] = rr;
+    }
+    return;
+  }
   for (int64_t blk = tl.E0; blk < tl.E1; blk += kWave) {
     const int64_t rem = tl.E1 - blk;
     const int n = rem < kWave ? static_cast<int>(rem) : kWave;
@@ -146,7 +155,10 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __re
   if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
-// Stable scatter of one tile by digit into its global slots.
+// Stable scatter of one tile by digit into its global slots.  The tile is
+// first reordered by digit in LDS, then written out with consecutive threads
+// on consecutive slots of a digit's run, so that stores coalesce.
+static_assert(kDigitsPerThread == 1, "one digit per thread in the scatter prologue");
 __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
@@ -154,67 +166,73 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint32_t* __restrict__ totals, const uint32_t* __restrict__ n_dev) {
   n = live_count(n, n_dev);
   // tiles wholly past the live keys hold nothing (their counts are zero)
-  if (static_cast<int64_t>(blockIdx.x) * kSortTile >= n) return;
+  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSortTile;
+  if (tile0 >= n) return;
+  const int in_tile = n - tile0 < kSortTile ? static_cast<int>(n - tile0) : kSortTile;
   __shared__ uint32_t cur[kWavesPerBlock][kBins];
+  __shared__ uint32_t gdst[kBins];  // global slot of the digit's run minus its LDS start
   __shared__ uint32_t wsum[kWavesPerBlock];
+  __shared__ uint32_t sk[kSortTile], sv[kSortTile];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&cur[0][0])[i] = 0;
   __syncthreads();
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile + w * kWaveSortKeys;
+  const int lbase = w * kWaveSortKeys;
   uint32_t k[kSortItemsPerLane], v[kSortItemsPerLane];
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
-    const int64_t idx = base + s * kWave + lane;
-    k[s] = idx < n ? keys_in[idx] : 0u;
-    v[s] = idx < n ? vals_in[idx] : 0u;
+    const int li = lbase + s * kWave + lane;
+    k[s] = li < in_tile ? keys_in[tile0 + li] : 0u;
+    v[s] = li < in_tile ? vals_in[tile0 + li] : 0u;
   }
   // per-wave digit counts
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
-    const bool valid = base + s * kWave + lane < n;
+    const bool valid = lbase + s * kWave + lane < in_tile;
     const uint32_t digit = (k[s] >> shift) & (kBins - 1);
     const uint64_t eq = match_digit(digit, valid);
     if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
   }
-  // First slot of each digit: exclusive scan of the digit totals; thread t
-  // owns digits [t*kDigitsPerThread, (t+1)*kDigitsPerThread).
-  const int d0 = threadIdx.x * kDigitsPerThread;
-  uint32_t tot[kDigitsPerThread];
-  uint32_t mine = 0;
-#pragma unroll
-  for (int i = 0; i < kDigitsPerThread; ++i) {
-    tot[i] = totals[d0 + i];
-    mine += tot[i];
-  }
-  uint32_t unused;
-  uint32_t digit_base = block_exclusive_scan(mine, wsum, &unused);
   __syncthreads();
-  // wave start offsets: global slot of the tile + counts of earlier waves
+  // thread d owns digit d: its LDS run starts after the tile's smaller
+  // digits; its global run after all smaller digits and earlier tiles
+  const int d = threadIdx.x;
+  uint32_t here = 0;
 #pragma unroll
-  for (int i = 0; i < kDigitsPerThread; ++i) {
-    const int d = d0 + i;
-    uint32_t run = digit_base + offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
-    digit_base += tot[i];
+  for (int ww = 0; ww < kWavesPerBlock; ++ww) here += cur[ww][d];
+  uint32_t unused;
+  const uint32_t local0 = block_exclusive_scan(here, wsum, &unused);
+  const uint32_t global0 = block_exclusive_scan(totals[d], wsum, &unused) +
+                           offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
+  gdst[d] = global0 - local0;  // modulo 2^32; slot = gdst + LDS index
+  uint32_t run = local0;
 #pragma unroll
-    for (int ww = 0; ww < kWavesPerBlock; ++ww) {
-      const uint32_t c = cur[ww][d];
-      cur[ww][d] = run;
-      run += c;
-    }
+  for (int ww = 0; ww < kWavesPerBlock; ++ww) {
+    const uint32_t c = cur[ww][d];
+    cur[ww][d] = run;
+    run += c;
   }
   __syncthreads();
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
-    const bool valid = base + s * kWave + lane < n;
+    const bool valid = lbase + s * kWave + lane < in_tile;
     const uint32_t digit = (k[s] >> shift) & (kBins - 1);
     const uint64_t eq = match_digit(digit, valid);
-    const uint32_t pos = cur[w][digit] + static_cast<uint32_t>(__popcll(eq & lanes_below(lane)));
-    if (valid && pos < n) {  // always true when the counts agree; guards memory anyway
-      keys_out[pos] = k[s];
-      vals_out[pos] = v[s];
+    if (valid) {
+      const uint32_t li = cur[w][digit] + static_cast<uint32_t>(__popcll(eq & lanes_below(lane)));
+      sk[li] = k[s];
+      sv[li] = v[s];
     }
     // all lanes have read cur[w][digit] above; group leaders advance it
     if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < in_tile; i += kBlockThreads) {
+    const uint32_t key = sk[i];
+    const uint32_t pos = gdst[(key >> shift) & (kBins - 1)] + static_cast<uint32_t>(i);
+    if (pos < n) {  // always true when the counts agree; guards memory anyway
+      keys_out[pos] = key;
+      vals_out[pos] = sv[i];
+    }
   }
 }
 

@@ -34,11 +34,13 @@ hipError_t launch_keygen(const KParams& p, const void* indices, const void* offs
 // Stable LSD radix sort of (keys, vals) by the low `bits` bits (8-bit
 // digits); on return keys/vals point at whichever buffer pair holds the
 // result.  scratch: radix_scratch_bytes(n) bytes.  With n_dev the number of
-// pairs is min(n, *n_dev) (read on the device; n sizes the launch).
+// pairs is min(n, *n_dev) (read on the device; n sizes the launch).  With
+// first_counted the first pass's per-tile digit counts are already at the
+// start of scratch (written while the keys were made).
 size_t radix_scratch_bytes(int64_t n);
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
                             int64_t n, int bits, uint32_t* scratch, hipStream_t stream,
-                            const uint32_t* n_dev = nullptr);
+                            const uint32_t* n_dev = nullptr, bool first_counted = false);
 // Bits of the item hash the grouping sort orders for N lookups.
 int grouping_bits(int64_t N);
 

@@ -136,6 +136,85 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
   }
 }
 
+// Keygen in item space for batches with as many items as bags, fused with
+// the first radix pass's histogram: workgroup blk takes the sort tile of
+// items [blk * kSortTile, ...), writes their (key, row) pairs and the tile's
+// digit counts of the low kSortBits bits (counts[d * nblocks + blk]).  When
+// every item of the tile is its own bag (offsets[e] == e), item e belongs
+// to bag e; otherwise each item finds its bag by binary search over the
+// offsets (the largest g with offsets[g] <= e).
+__global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
+    const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
+    uint32_t* __restrict__ keys, uint32_t* __restrict__ rows, float* __restrict__ inv_len,
+    uint32_t* __restrict__ counts, const uint32_t nblocks) {
+  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSortTile;
+  const int in_tile = p.N - tile0 < kSortTile ? static_cast<int>(p.N - tile0) : kSortTile;
+  __shared__ uint32_t hist[kWavesPerBlock][kBins];
+  __shared__ int irregular;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
+  if (threadIdx.x == 0) irregular = 0;
+  __syncthreads();
+  const int lbase = w * kWaveSortKeys;
+  bool mine_ok = true;
+#pragma unroll
+  for (int s = 0; s < kSortItemsPerLane; ++s) {
+    const int li = lbase + s * kWave + lane;
+    if (li < in_tile) {
+      const int64_t e = tile0 + li;
+      if (load_offset(offsets, static_cast<uint64_t>(e), p.idx32) != e) mine_ok = false;
+    }
+  }
+  if (threadIdx.x == 0) {
+    const int64_t end = tile0 + in_tile;
+    if (load_offset(offsets, static_cast<uint64_t>(end), p.idx32) != end) mine_ok = false;
+  }
+  if (!mine_ok) irregular = 1;
+  __syncthreads();
+  const bool onehot = irregular == 0;
+#pragma unroll
+  for (int s = 0; s < kSortItemsPerLane; ++s) {
+    const int li = lbase + s * kWave + lane;
+    const bool valid = li < in_tile;
+    uint32_t digit = 0;
+    if (valid) {
+      const int64_t e = tile0 + li;
+      uint64_t g = static_cast<uint64_t>(e);
+      float il = 1.f;
+      bool first = true;
+      if (!onehot) {
+        uint64_t lo = 0, hi = p.num_bags - 1;  // largest g with offsets[g] <= e
+        while (lo < hi) {
+          const uint64_t mid = (lo + hi + 1) >> 1;
+          if (load_offset(offsets, mid, p.idx32) <= e) lo = mid; else hi = mid - 1;
+        }
+        g = lo;
+        const int64_t s0 = load_offset(offsets, g, p.idx32);
+        const int64_t s1 = load_offset(offsets, g + 1, p.idx32);
+        first = s0 == e;
+        il = s1 > s0 ? 1.f / static_cast<float>(s1 - s0) : 1.f;
+      }
+      const uint32_t t = static_cast<uint32_t>(g / p.B);
+      const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
+      const uint32_t r = b * p.T + t;
+      const uint32_t key = item_hash(load_index(indices, e, p.idx32), t * p.C, p.TC, p.a, p.b);
+      keys[e] = key;
+      rows[e] = r;
+      if (p.mean && first) inv_len[r] = il;
+      digit = key & (kBins - 1);
+    }
+    const uint64_t eq = match_digit(digit, valid);
+    if (valid && (eq & lanes_below(lane)) == 0) hist[w][digit] += __popcll(eq);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int ww = 0; ww < kWavesPerBlock; ++ww) c += hist[ww][d];
+    counts[static_cast<uint64_t>(d) * nblocks + blockIdx.x] = c;
+  }
+}
+
 // Row d of counts (one digit, nblocks entries): exclusive scan in place;
 // totals[d] = the row's sum.  One workgroup per digit.
 __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __restrict__ counts,
@@ -477,14 +556,15 @@ size_t sorted_workspace_bytes(const KParams& p) {
 
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
                             int64_t n, int bits, uint32_t* scratch, hipStream_t stream,
-                            const uint32_t* n_dev) {
+                            const uint32_t* n_dev, bool first_counted) {
   if (n == 0) return hipSuccess;
   const uint32_t nblocks = static_cast<uint32_t>((n + kSortTile - 1) / kSortTile);
   uint32_t* counts = scratch;
   uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
   for (int shift = 0; shift < bits; shift += kSortBits) {
-    hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys, n,
-                       shift, counts, nblocks, n_dev);
+    if (shift > 0 || !first_counted)
+      hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys, n,
+                         shift, counts, nblocks, n_dev);
     hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
                        nblocks, totals);
     hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys,
@@ -563,8 +643,20 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   float* inv_len = p.mean ? reinterpret_cast<float*>(
                                 reinterpret_cast<char*>(scratch) + radix_scratch_bytes(N))
                           : nullptr;
-  hipError_t e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);
-  if (e == hipSuccess) e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), scratch, stream);
+  // As many items as bags (one-hot batches): keygen in item space, fused
+  // with the first pass's histogram.
+  const bool item_space = static_cast<uint64_t>(N) == p.num_bags;
+  hipError_t e = hipSuccess;
+  if (item_space) {
+    const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
+    hipLaunchKernelGGL(keygen_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, p,
+                       indices, offsets, k0, v0, inv_len, scratch, nblocks);
+    e = hipGetLastError();
+  } else {
+    e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);
+  }
+  if (e == hipSuccess)
+    e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), scratch, stream, nullptr, item_space);
   if (e != hipSuccess) return e;
   if (p.rows_bf16)
     return launch_reduce_g(dst, scale, p, k0, v0, static_cast<const uint16_t*>(grad), inv_len,

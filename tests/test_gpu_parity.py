@@ -211,3 +211,47 @@ def test_microbenchmark_shape_counts(Z, variant):
     L.backward(ones, lr=1.0)
     _, _, _, _, cnt = L.ref_backward(ones, lr=1.0)
     assert np.array_equal(L.weights(), -cnt.astype(np.float32))
+
+
+def _irregular_equal_count(wl, B, seed=5):
+    """As many items as bags, but not one per bag: starting from one item per
+    bag, 1500 items move between random bags inside bags [5000, 9000), which
+    leaves the sort tiles before and after that range one-hot and the tiles
+    inside it irregular (bags of 0 .. several items)."""
+    nb = wl.T * B
+    rng = np.random.default_rng(seed)
+    lens = np.ones(nb, dtype=np.int64)
+    lo, hi = min(5000, nb - 2), min(9000, nb)
+    for _ in range(1500):
+        i, j = rng.integers(lo, hi, 2)
+        if lens[j] > 0 and i != j:
+            lens[i] += 1
+            lens[j] -= 1
+    offsets = np.zeros(nb + 1, dtype=np.int64)
+    np.cumsum(lens, out=offsets[1:])
+    assert offsets[-1] == nb
+    card = int(wl.cardinality.split(":")[1]) if wl.cardinality.startswith("fixed") else 1000
+    indices = rng.integers(0, card, nb, dtype=np.int64)
+    return synth.Inputs(indices=indices, offsets=offsets, B=B)
+
+
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
+@pytest.mark.parametrize("opt,mean", [("sgd", False), ("adagrad", True)])
+def test_irregular_bags_with_one_item_per_bag_on_average(variant, opt, mean):
+    """A batch with as many items as bags takes the one-hot paths (keygen in
+    item space fused with the first radix histogram); tiles whose bags are
+    not one item each fall back to finding each item's bag by search."""
+    wl = synth.get("c2").scaled(optimizer=opt, lr=0.05, M=1_000_000)
+    B = 700
+    L = Layer(wl, B=B, flags=VARIANTS[variant], mean=mean, s0=0.1 if opt == "adagrad" else 0.0)
+    L.x = _irregular_equal_count(wl, B)
+    L.indices = torch.from_numpy(L.x.indices).to(L.dev)
+    L.offsets = torch.from_numpy(L.x.offsets).to(L.dev)
+    got = L.forward()
+    ref, s_abs = L.ref_forward()
+    parity.check_forward(got, ref, s_abs, 1e-5)
+    g = synth.make_grad(wl, B=B)
+    L.backward(g)
+    w_ref, s_ref, G, A, _ = L.ref_backward(g)
+    s_gpu = None if L.state is None else L.state.cpu().numpy()
+    parity.check_update(L, L.weights(), s_gpu, w_ref, s_ref, G, A, wl.lr)

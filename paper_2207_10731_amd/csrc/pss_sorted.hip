@@ -157,11 +157,15 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
   __syncthreads();
   const int lbase = w * kWaveSortKeys;
   bool mine_ok = true;
+  // an item's index does not depend on its bag: load both in one round trip
+  uint32_t ix[kSortItemsPerLane];
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
     const int li = lbase + s * kWave + lane;
+    ix[s] = 0;
     if (li < in_tile) {
       const int64_t e = tile0 + li;
+      ix[s] = load_index(indices, e, p.idx32);
       if (load_offset(offsets, static_cast<uint64_t>(e), p.idx32) != e) mine_ok = false;
     }
   }
@@ -197,7 +201,7 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
       const uint32_t t = static_cast<uint32_t>(g / p.B);
       const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
       const uint32_t r = b * p.T + t;
-      const uint32_t key = item_hash(load_index(indices, e, p.idx32), t * p.C, p.TC, p.a, p.b);
+      const uint32_t key = item_hash(ix[s], t * p.C, p.TC, p.a, p.b);
       keys[e] = key;
       rows[e] = r;
       if (p.mean && first) inv_len[r] = il;
@@ -217,18 +221,32 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
 
 // Row d of counts (one digit, nblocks entries): exclusive scan in place;
 // totals[d] = the row's sum.  One workgroup per digit.
+constexpr int kScanPerThread = 16;
 __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __restrict__ counts,
                                                                   const uint32_t nblocks,
                                                                   uint32_t* __restrict__ totals) {
   __shared__ uint32_t wsum[kWavesPerBlock];
   uint32_t* row = counts + static_cast<uint64_t>(blockIdx.x) * nblocks;
+  // entries per thread for this row (at most kScanPerThread per round)
+  const uint32_t per = (nblocks + kBlockThreads - 1) / kBlockThreads;
+  const uint32_t pt = per < kScanPerThread ? per : kScanPerThread;
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < nblocks; base += kBlockThreads) {
-    const uint32_t i = base + threadIdx.x;
-    const uint32_t v = i < nblocks ? row[i] : 0u;
+  for (uint32_t base = 0; base < nblocks; base += pt * kBlockThreads) {
+    const uint32_t i0 = base + threadIdx.x * pt;
+    uint32_t v[kScanPerThread];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPerThread; ++j) {
+      v[j] = (static_cast<uint32_t>(j) < pt && i0 + j < nblocks) ? row[i0 + j] : 0u;
+      sum += v[j];
+    }
     uint32_t tot;
-    const uint32_t ex = block_exclusive_scan(v, wsum, &tot);
-    if (i < nblocks) row[i] = carry + ex;
+    uint32_t run = carry + block_exclusive_scan(sum, wsum, &tot);
+#pragma unroll
+    for (int j = 0; j < kScanPerThread; ++j) {
+      if (static_cast<uint32_t>(j) < pt && i0 + j < nblocks) row[i0 + j] = run;
+      run += v[j];
+    }
     carry += tot;
   }
   if (threadIdx.x == 0) totals[blockIdx.x] = carry;

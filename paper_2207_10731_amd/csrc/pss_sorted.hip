@@ -407,11 +407,13 @@ __device__ __forceinline__ void load_rows(float (&g)[U][EPL], const GT* __restri
 }
 
 // Sums the rows of positions q .. q+U-1 into acc; every run that ends there
-// goes to the buffer (values, key); returns the number of runs written.
+// goes to the buffer (values, key), except the quarter's first run while
+// `head` is set (it continues a run of the previous quarter): that one goes
+// to headv and clears `head`.  Returns the number of runs put in the buffer.
 template <int EPL, int U>
 __device__ __forceinline__ int sum_runs(const float (&g)[U][EPL], float* acc, uint32_t wk, int q,
                                         int nq, uint32_t after, float* vals, uint32_t* rkeys,
-                                        int lane) {
+                                        bool& head, float* headv, int lane) {
   int nrun = 0;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -421,17 +423,41 @@ __device__ __forceinline__ int sum_runs(const float (&g)[U][EPL], float* acc, ui
       const uint32_t h = readlane_u32(wk, q + u);
       const uint32_t hn = q + u + 1 < nq ? readlane_u32(wk, q + u + 1) : after;
       if (hn != h) {
+        float* dstv = head ? headv : vals + nrun * (kWave * EPL);
 #pragma unroll
         for (int r = 0; r < EPL; ++r) {
-          vals[nrun * (kWave * EPL) + kWave * r + lane] = acc[r];
+          dstv[kWave * r + lane] = acc[r];
           acc[r] = 0.f;
         }
-        if (lane == 0) rkeys[nrun] = h;
-        ++nrun;
+        if (head) {
+          head = false;
+        } else {
+          if (lane == 0) rkeys[nrun] = h;
+          ++nrun;
+        }
       }
     }
   }
   return nrun;
+}
+
+// Adds scale * v (lane's EPL values of the run with item hash h) at the
+// run's hashed addresses.
+template <int EPL, bool SIGN>
+__device__ __forceinline__ void deposit_run(float* __restrict__ dst, float scale, const KParams& p,
+                                            uint32_t h, const float* v, const bool* act,
+                                            const uint32_t* step, const uint32_t* step2,
+                                            const uint32_t* kk) {
+  const uint32_t h20 = SIGN ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) {
+    if (!act[r]) continue;
+    const uint32_t ent = chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M),
+                                           add_mod_p(h20, step2[r]), p);
+    const Elem el = elem_of<SIGN>(ent, kk[r], p.M);
+    const float x = scale * v[r];
+    if (!SIGN || el.read) unsafeAtomicAdd(dst + el.m, SIGN ? apply_sign(x, el) : x);
+  }
 }
 
 template <int EPL, int U, bool SIGN, typename GT>
@@ -448,11 +474,25 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
   if (p0 >= n) return;  // whole workgroup
   const int cnt = n - p0 < kPiece ? static_cast<int>(n - p0) : kPiece;
   const uint32_t c0 = blockIdx.y * (kWave * EPL);
-  __shared__ uint32_t lk[kPiece], lr[kPiece];  // the readers' sorted lists
-  __shared__ uint32_t mk[kPiece], mr[kPiece];  // merged order
+  // The readers' sorted lists and the merged order; once every reader holds
+  // its quarter in registers the same LDS takes the partial sums of runs
+  // that cross a quarter boundary (headv: the part in the quarter where the
+  // run ends, tailv: the part in the quarter it leaves).
+  constexpr int kRowF = kWave * EPL;
+  constexpr int kSortWords = 4 * kPiece;
+  constexpr int kPartWords = 2 * kReaders * kRowF;
+  __shared__ uint32_t sortbuf[kSortWords > kPartWords ? kSortWords : kPartWords];
+  uint32_t* lk = sortbuf;
+  uint32_t* lr = sortbuf + kPiece;
+  uint32_t* mk = sortbuf + 2 * kPiece;
+  uint32_t* mr = sortbuf + 3 * kPiece;
+  float* headv = reinterpret_cast<float*>(sortbuf);
+  float* tailv = headv + kReaders * kRowF;
   __shared__ float vals[kReaders][2][kSlotFloats];
   __shared__ uint32_t rkeys[kReaders][2][U];
   __shared__ int nruns[kReaders][2];
+  __shared__ uint32_t qkey[kReaders];  // key at the start of each quarter
+  __shared__ int qflags[kReaders];     // bit 0: tail open, bit 1: through (no run ends inside)
 
   bool act[EPL];
 #pragma unroll
@@ -485,16 +525,28 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
   lds_barrier();
 
   // 3. phases: reader sums batch k into buffer k&1, depositor drains the
-  //    other buffer.  Every wavefront runs the same number of phases.
+  //    other buffer.  Every wavefront runs the same number of phases.  A run
+  //    that crosses from one quarter into the next is not cut: its part in
+  //    each quarter goes to tailv / headv and is deposited once at the end.
   const int q0 = pair * kWave;
   const int nq = cnt - q0 < kWave ? (cnt - q0 > 0 ? cnt - q0 : 0) : kWave;
   constexpr int kBatches = kWave / U;
+  uint32_t wk = 0xffffffffu, wr = 0;
+  bool head_open = false, tail_open = false;
+  uint32_t after = 0xffffffffu;
   if (reader && nq > 0) {
-    const uint32_t wk = mk[my];
-    const uint32_t wr = mr[my];
-    // key after the quarter: a run that continues into the next quarter is
-    // cut here (it deposits once per quarter)
-    const uint32_t after = 0xffffffffu;
+    wk = mk[my];
+    wr = mr[my];
+    head_open = q0 > 0 && mk[q0] == mk[q0 - 1];
+    if (q0 + nq < cnt && mk[q0 + nq] == mk[q0 + nq - 1]) {
+      tail_open = true;
+      after = mk[q0 + nq];  // the run goes on past the quarter
+    }
+    if (lane == 0) qkey[pair] = mk[q0];
+  }
+  lds_barrier();  // every reader holds its quarter: the sort buffers are free
+  if (reader && nq > 0) {
+    bool head = head_open;
     float acc[EPL];
 #pragma unroll
     for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
@@ -512,12 +564,21 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
           else load_rows<EPL, U>(gb, grad, inv_len, p, wr, q + U, nq, c0, lane, act);
         }
         int nr = 0;
+        float* hv = headv + pair * kRowF;
         if (q < nq)
           nr = (k & 1) ? sum_runs<EPL, U>(gb, acc, wk, q, nq, after, vals[pair][k & 1],
-                                          rkeys[pair][k & 1], lane)
+                                          rkeys[pair][k & 1], head, hv, lane)
                        : sum_runs<EPL, U>(ga, acc, wk, q, nq, after, vals[pair][k & 1],
-                                          rkeys[pair][k & 1], lane);
+                                          rkeys[pair][k & 1], head, hv, lane);
         if (lane == 0) nruns[pair][k & 1] = nr;
+      } else {
+        // the open run's part in this quarter (with no run ending inside,
+        // the quarter lies wholly within one run: "through")
+        if (tail_open) {
+#pragma unroll
+          for (int r = 0; r < EPL; ++r) tailv[pair * kRowF + kWave * r + lane] = acc[r];
+        }
+        if (lane == 0) qflags[pair] = (tail_open ? 1 : 0) | (head ? 2 : 0);
       }
       lds_barrier();
     }
@@ -525,6 +586,7 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
 #pragma unroll
     for (int k = 0; k <= kBatches; ++k) {
       if (k < kBatches && lane == 0) nruns[pair][k & 1] = 0;
+      if (k == kBatches && lane == 0) qflags[pair] = 0;
       lds_barrier();
     }
   } else {
@@ -543,20 +605,32 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
         const int b = (k - 1) & 1;
         const int nr = nruns[pair][b];
         for (int s = 0; s < nr; ++s) {
-          const uint32_t h = rkeys[pair][b][s];
-          const uint32_t h20 = SIGN ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
+          float v[EPL];
 #pragma unroll
-          for (int r = 0; r < EPL; ++r) {
-            if (!act[r]) continue;
-            const uint32_t ent = chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M),
-                                                   add_mod_p(h20, step2[r]), p);
-            const Elem el = elem_of<SIGN>(ent, kk[r], p.M);
-            const float v = scale * vals[pair][b][s * (kWave * EPL) + kWave * r + lane];
-            if (!SIGN || el.read) unsafeAtomicAdd(dst + el.m, SIGN ? apply_sign(v, el) : v);
-          }
+          for (int r = 0; r < EPL; ++r) v[r] = vals[pair][b][s * kRowF + kWave * r + lane];
+          deposit_run<EPL, SIGN>(dst, scale, p, rkeys[pair][b][s], v, act, step, step2, kk);
         }
       }
       lds_barrier();
+    }
+    // Runs crossing quarter boundaries: depositor `pair` takes the run that
+    // leaves quarter `pair` (unless quarter `pair` lies inside a run that
+    // began earlier) and adds the parts of every quarter it passes through
+    // and of the quarter where it ends.
+    const int fl = qflags[pair];
+    if ((fl & 1) && !(fl & 2)) {
+      float v[EPL];
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) v[r] = tailv[pair * kRowF + kWave * r + lane];
+      int q = pair + 1;
+      while (q < kReaders - 1 && (qflags[q] & 3) == 3) {  // through quarters
+#pragma unroll
+        for (int r = 0; r < EPL; ++r) v[r] += tailv[q * kRowF + kWave * r + lane];
+        ++q;
+      }
+#pragma unroll
+      for (int r = 0; r < EPL; ++r) v[r] += headv[q * kRowF + kWave * r + lane];
+      deposit_run<EPL, SIGN>(dst, scale, p, qkey[q], v, act, step, step2, kk);
     }
   }
 }

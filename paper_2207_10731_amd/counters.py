@@ -1,12 +1,12 @@
-"""Cache and atomic counters of the two dominant kernels, summarised.
+"""Cache and atomic counters of the library's kernels, summarised.
 
   python -m paper_2207_10731_amd.counters --out profiles/cache_atomics_c2.md DB1 DB2 ...
 
 Each DB is a rocprofv3 result database of one --pmc pass over the same
-command (counters differ per pass).  For forward_kernel and
-reduce_deposit_kernel it prints the per-dispatch average of every counter
-found, and the derived L2 hit rate, L2-to-fabric bytes and atomic requests
-per lookup.
+command (counters differ per pass).  For each kernel named by --kernels
+(default: forward_kernel and reduce_deposit_kernel) it prints the
+per-dispatch average of every counter found, and the derived L2 hit rate
+and atomic requests per lookup.
 """
 from __future__ import annotations
 
@@ -17,14 +17,14 @@ from collections import defaultdict
 KERNELS = ("forward_kernel", "reduce_deposit_kernel")
 
 
-def collect(dbs):
+def collect(dbs, kernels=KERNELS):
     vals = defaultdict(dict)
     for db in dbs:
         c = sqlite3.connect(db)
         for name, counter, avg in c.execute(
                 "select kernel_name, counter_name, avg(value) from counters_collection "
                 "group by kernel_name, counter_name"):
-            for k in KERNELS:
+            for k in kernels:
                 if f"pss::{k}<" in name or f"pss::{k}(" in name:
                     vals[k][counter] = avg
     return vals
@@ -36,15 +36,18 @@ def main(argv=None):
     ap.add_argument("--lookups", type=float, default=1703936.0)
     ap.add_argument("--command", default="")
     ap.add_argument("--out", default=None)
+    ap.add_argument("--kernels", default=",".join(KERNELS),
+                    help="comma-separated kernel names (without the pss:: prefix)")
     a = ap.parse_args(argv)
-    vals = collect(a.dbs)
-    lines = ["| counter (per dispatch) | " + " | ".join(KERNELS) + " |",
-             "|---|" + "---|" * len(KERNELS)]
-    names = sorted({n for k in KERNELS for n in vals[k]})
+    kernels = tuple(k for k in a.kernels.split(",") if k)
+    vals = collect(a.dbs, kernels)
+    lines = ["| counter (per dispatch) | " + " | ".join(kernels) + " |",
+             "|---|" + "---|" * len(kernels)]
+    names = sorted({n for k in kernels for n in vals[k]})
     for n in names:
-        lines.append(f"| {n} | " + " | ".join(f"{vals[k].get(n, float('nan')):,.0f}" for k in KERNELS) + " |")
+        lines.append(f"| {n} | " + " | ".join(f"{vals[k].get(n, float('nan')):,.0f}" for k in kernels) + " |")
     derived = []
-    for k in KERNELS:
+    for k in kernels:
         v = vals[k]
         if "TCC_HIT_sum" in v and "TCC_MISS_sum" in v:
             tot = v["TCC_HIT_sum"] + v["TCC_MISS_sum"]

@@ -42,12 +42,13 @@ template <typename WT, int EPL, int U, bool SIGN>
 __device__ __forceinline__ void forward_onehot_tile(
     const WT* __restrict__ w, const KParams& p, const Tile& tl, const void* __restrict__ indices,
     void* __restrict__ out, uint32_t* tab, int lane, uint32_t c0, const uint32_t* jj,
-    const uint32_t* kk, const bool* act) {
+    const uint32_t* kk, const bool* act, uint32_t spec) {
   const int nb = tl.nb;
   uint32_t key = 0xffffffffu;  // empty lanes sort last
   uint32_t bag = static_cast<uint32_t>(lane);
+  const bool hit = tl.E0 == static_cast<int64_t>(tl.g0);
   if (lane < nb) {
-    const uint32_t i = load_index(indices, tl.E0 + lane, p.idx32);
+    const uint32_t i = hit ? spec : load_index(indices, tl.E0 + lane, p.idx32);
     key = item_hash(i, tl.tC, p.TC, p.a, p.b);
   }
   wave_sort_pairs(key, bag, lane);
@@ -116,13 +117,17 @@ __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     step2[r] = (TAB || !SIGN) ? 0u : chunk_step(p.a2, jj[r]);
   }
 
+  // One-hot batches: item g0 + lane is usually bag g0 + lane's item; its
+  // index is requested together with the offsets.
+  uint32_t spec = 0;
+  if (TAB && static_cast<int64_t>(g0) + lane < p.N) spec = load_index(indices, g0 + lane, p.idx32);
   const Tile tl = load_tile(p, offsets, g0, lane);
 
   if (TAB) {
     // One-hot tile (every bag exactly one item): gather each distinct token
     // of the tile once and store its row to every bag that reads it.
     if (__ballot(lane >= tl.nb || tl.len == 1) == ~0ull) {
-      forward_onehot_tile<WT, EPL, U, SIGN>(w, p, tl, indices, out, tab, lane, c0, jj, kk, act);
+      forward_onehot_tile<WT, EPL, U, SIGN>(w, p, tl, indices, out, tab, lane, c0, jj, kk, act, spec);
       return;
     }
   }

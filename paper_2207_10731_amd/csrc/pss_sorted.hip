@@ -136,6 +136,13 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
   }
 }
 
+// indices[e] / offsets[g] with the integer width fixed at compile time.
+template <bool I32>
+__device__ __forceinline__ int64_t load_int(const void* a, uint64_t i) {
+  if constexpr (I32) return __builtin_nontemporal_load(static_cast<const int32_t*>(a) + i);
+  else return __builtin_nontemporal_load(static_cast<const int64_t*>(a) + i);
+}
+
 // Keygen in item space for batches with as many items as bags, fused with
 // the first radix pass's histogram: workgroup blk takes the sort tile of
 // items [blk * kSortTile, ...), writes their (key, row) pairs and the tile's
@@ -143,6 +150,7 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
 // every item of the tile is its own bag (offsets[e] == e), item e belongs
 // to bag e; otherwise each item finds its bag by binary search over the
 // offsets (the largest g with offsets[g] <= e).
+template <bool I32>
 __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
     uint32_t* __restrict__ keys, uint32_t* __restrict__ rows, float* __restrict__ inv_len,
@@ -152,27 +160,32 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
   __shared__ uint32_t hist[kWavesPerBlock][kBins];
   __shared__ int irregular;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
-  for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
-  if (threadIdx.x == 0) irregular = 0;
-  __syncthreads();
   const int lbase = w * kWaveSortKeys;
-  bool mine_ok = true;
-  // an item's index does not depend on its bag: load both in one round trip
+  // Every index and offset of the thread is requested before any is used:
+  // one wait for memory per thread.  An item's index does not depend on its
+  // bag.
   uint32_t ix[kSortItemsPerLane];
+  int64_t ofs[kSortItemsPerLane];
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
     const int li = lbase + s * kWave + lane;
+    const int64_t e = tile0 + li;
     ix[s] = 0;
+    ofs[s] = e;
     if (li < in_tile) {
-      const int64_t e = tile0 + li;
-      ix[s] = load_index(indices, e, p.idx32);
-      if (load_offset(offsets, static_cast<uint64_t>(e), p.idx32) != e) mine_ok = false;
+      ix[s] = static_cast<uint32_t>(load_int<I32>(indices, static_cast<uint64_t>(e)));
+      ofs[s] = load_int<I32>(offsets, static_cast<uint64_t>(e));
     }
   }
-  if (threadIdx.x == 0) {
-    const int64_t end = tile0 + in_tile;
-    if (load_offset(offsets, static_cast<uint64_t>(end), p.idx32) != end) mine_ok = false;
-  }
+  const int64_t end = tile0 + in_tile;
+  const int64_t oend = threadIdx.x == 0 ? load_int<I32>(offsets, static_cast<uint64_t>(end)) : end;
+  for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
+  if (threadIdx.x == 0) irregular = 0;
+  __syncthreads();
+  bool mine_ok = oend == end;
+#pragma unroll
+  for (int s = 0; s < kSortItemsPerLane; ++s)
+    if (ofs[s] != tile0 + lbase + s * kWave + lane) mine_ok = false;
   if (!mine_ok) irregular = 1;
   __syncthreads();
   const bool onehot = irregular == 0;
@@ -183,23 +196,24 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     uint32_t digit = 0;
     if (valid) {
       const int64_t e = tile0 + li;
-      uint64_t g = static_cast<uint64_t>(e);
+      // bag numbers are below 2^32
+      uint32_t g = static_cast<uint32_t>(e);
       float il = 1.f;
       bool first = true;
       if (!onehot) {
         uint64_t lo = 0, hi = p.num_bags - 1;  // largest g with offsets[g] <= e
         while (lo < hi) {
           const uint64_t mid = (lo + hi + 1) >> 1;
-          if (load_offset(offsets, mid, p.idx32) <= e) lo = mid; else hi = mid - 1;
+          if (load_int<I32>(offsets, mid) <= e) lo = mid; else hi = mid - 1;
         }
-        g = lo;
-        const int64_t s0 = load_offset(offsets, g, p.idx32);
-        const int64_t s1 = load_offset(offsets, g + 1, p.idx32);
+        g = static_cast<uint32_t>(lo);
+        const int64_t s0 = load_int<I32>(offsets, lo);
+        const int64_t s1 = load_int<I32>(offsets, lo + 1);
         first = s0 == e;
         il = s1 > s0 ? 1.f / static_cast<float>(s1 - s0) : 1.f;
       }
-      const uint32_t t = static_cast<uint32_t>(g / p.B);
-      const uint32_t b = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B);
+      const uint32_t t = g / p.B;
+      const uint32_t b = g - t * p.B;
       const uint32_t r = b * p.T + t;
       const uint32_t key = item_hash(ix[s], t * p.C, p.TC, p.a, p.b);
       keys[e] = key;
@@ -274,6 +288,11 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&cur[0][0])[i] = 0;
   __syncthreads();
   const int lbase = w * kWaveSortKeys;
+  // thread d owns digit d: its totals and this tile's offset are requested
+  // with the tile's pairs (one wait for memory)
+  const int d = threadIdx.x;
+  const uint32_t total_d = totals[d];
+  const uint32_t offset_d = offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
   uint32_t k[kSortItemsPerLane], v[kSortItemsPerLane];
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
@@ -290,16 +309,14 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     if (valid && (eq & lanes_below(lane)) == 0) cur[w][digit] += __popcll(eq);
   }
   __syncthreads();
-  // thread d owns digit d: its LDS run starts after the tile's smaller
-  // digits; its global run after all smaller digits and earlier tiles
-  const int d = threadIdx.x;
+  // digit d's LDS run starts after the tile's smaller digits; its global
+  // run after all smaller digits and earlier tiles
   uint32_t here = 0;
 #pragma unroll
   for (int ww = 0; ww < kWavesPerBlock; ++ww) here += cur[ww][d];
   uint32_t unused;
   const uint32_t local0 = block_exclusive_scan(here, wsum, &unused);
-  const uint32_t global0 = block_exclusive_scan(totals[d], wsum, &unused) +
-                           offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
+  const uint32_t global0 = block_exclusive_scan(total_d, wsum, &unused) + offset_d;
   gdst[d] = global0 - local0;  // modulo 2^32; slot = gdst + LDS index
   uint32_t run = local0;
 #pragma unroll
@@ -741,8 +758,12 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   hipError_t e = hipSuccess;
   if (item_space) {
     const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
-    hipLaunchKernelGGL(keygen_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, p,
-                       indices, offsets, k0, v0, inv_len, scratch, nblocks);
+    if (p.idx32)
+      hipLaunchKernelGGL(keygen_hist_kernel<true>, dim3(nblocks), dim3(kBlockThreads), 0, stream,
+                         p, indices, offsets, k0, v0, inv_len, scratch, nblocks);
+    else
+      hipLaunchKernelGGL(keygen_hist_kernel<false>, dim3(nblocks), dim3(kBlockThreads), 0, stream,
+                         p, indices, offsets, k0, v0, inv_len, scratch, nblocks);
     e = hipGetLastError();
   } else {
     e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);

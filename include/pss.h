@@ -95,8 +95,8 @@ enum {
  *   SORTED  lookups are grouped by token (radix sort on the item hash), the
  *           output-gradient rows of each token are summed in registers, and
  *           each token's sum is added once at its hashed addresses (float
- *           atomics; a token whose lookups span several 64-pair quarters of
- *           the 256-pair pieces adds one partial sum per quarter).
+ *           atomics; a token whose lookups span several of the 256-pair
+ *           pieces of the grouped order adds one partial sum per piece).
  *   SPARSE  Alg. 1 sparse branch: the unique locations and summed values of
  *           pss_gradient_sparse, then the optimizer applied at those
  *           locations only.  No float atomics: bit-identical run to run.

@@ -20,7 +20,7 @@ hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, cons
 
 // Sorted deposit: lookups grouped by token (radix sort on the item hash),
 // gradient rows summed per token, one deposit of scale * sum per token and
-// 64-pair quarter of a 256-pair piece.  `workspace` must hold
+// 256-pair piece of the grouped order.  `workspace` must hold
 // sorted_workspace_bytes(p) bytes.
 size_t sorted_workspace_bytes(const KParams& p);
 hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,

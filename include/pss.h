@@ -49,8 +49,13 @@
  *   load and rounded to nearest-even once per update.
  * Memory.  Every array argument is device memory owned by the caller; the
  *   library keeps no pointer after the call returns other than in the work it
- *   enqueued.  Scratch space is taken stream-ordered from a library-owned
- *   memory pool on the current device and returned on the same stream.
+ *   enqueued.  Scratch space of the backward and sparse-gradient calls is a
+ *   library-owned device buffer kept per (device, stream) between calls and
+ *   grown to the largest call made on that stream (taken from a
+ *   library-owned memory pool); pss_release_scratch returns these buffers.
+ *   While `stream` is being captured into a graph, scratch is allocated
+ *   stream-ordered from the pool and freed on the same stream instead, so
+ *   that the graph owns it.
  * Streams.  Work is enqueued on `stream` (0 = the legacy default stream) of
  *   the current device; calls return once the work is enqueued.
  * Errors.  Arguments are checked on the host before anything is enqueued; a
@@ -222,6 +227,13 @@ int pss_hash_signs_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
 int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N);
 
 /* Static, NUL-terminated description of a status code. */
+/* Frees the scratch buffers kept between calls (see "Memory" above) on
+ * every device that holds one, after waiting for that device's work to
+ * finish.  Host only; no call of this library may be in progress on another
+ * thread.  Later calls allocate afresh.  Returns PSS_ERR_HIP if a runtime
+ * call fails (the buffers are forgotten either way). */
+int pss_release_scratch(void);
+
 const char* pss_status_string(int status);
 
 #ifdef __cplusplus

@@ -137,6 +137,61 @@ int scratch_alloc(void** ptr, size_t bytes, hipStream_t stream) {
   return st == hipSuccess ? PSS_OK : PSS_ERR_HIP;
 }
 
+// Scratch kept between calls, one buffer per (device, stream), as large as
+// the largest call on that stream so far.  A pool allocation and its
+// stream-ordered free per call cost the stream a marker between steps and
+// block the host until earlier frees have completed; a kept buffer costs
+// neither.  Work on one stream runs in order, so consecutive calls on it
+// may share the buffer.  Streams are told apart by handle: the runtime
+// keeps a stream object (whose address is the handle) alive while commands
+// enqueued on it are pending, so a handle is reused only after the work of
+// the stream it named has finished.
+struct KeptScratch {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_kept_mu;
+std::map<std::pair<int, uintptr_t>, KeptScratch> g_kept;
+
+// Scratch of `bytes` for work enqueued on `stream`.  *kept says whether it
+// is a kept buffer (nothing to return) or a pool allocation that the caller
+// returns with hipFreeAsync on the stream after enqueueing its work: so it
+// is while the stream is being captured into a graph (the graph then owns
+// its allocation, and replays on other streams cannot share a kept buffer)
+// or when the capture status cannot be read.
+int stream_scratch(void** ptr, size_t bytes, hipStream_t stream, bool* kept) {
+  *kept = false;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  int dev = 0;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone ||
+      hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return scratch_alloc(ptr, bytes, stream);
+  }
+  std::lock_guard<std::mutex> lock(g_kept_mu);
+  KeptScratch& k = g_kept[{dev, reinterpret_cast<uintptr_t>(stream)}];
+  if (k.bytes < bytes) {
+    // the smaller buffer goes back to the pool after the work already
+    // enqueued on the stream
+    if (k.ptr != nullptr && hipFreeAsync(k.ptr, stream) != hipSuccess) return PSS_ERR_HIP;
+    k.ptr = nullptr;
+    k.bytes = 0;
+    void* p = nullptr;
+    const int st = scratch_alloc(&p, bytes, stream);
+    if (st != PSS_OK) return st;
+    k.ptr = p;
+    k.bytes = bytes;
+  }
+  *ptr = k.ptr;
+  *kept = true;
+  return PSS_OK;
+}
+
+// Returns scratch from stream_scratch: pool allocations go back on the stream.
+hipError_t stream_scratch_done(void* ptr, bool kept, hipStream_t stream) {
+  return (ptr == nullptr || kept) ? hipSuccess : hipFreeAsync(ptr, stream);
+}
+
 int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; }
 
 uint64_t splitmix64_next(uint64_t* state) {
@@ -200,13 +255,14 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
     // optimizer applied at each location as it is summed.
     const size_t ws_bytes = pss::sparse_workspace_bytes(p);
     void* ws = nullptr;
-    st = scratch_alloc(&ws, 256 + ws_bytes, stream);
+    bool kept = false;
+    st = stream_scratch(&ws, 256 + ws_bytes, stream, &kept);
     if (st != PSS_OK) return st;
     uint32_t* count = static_cast<uint32_t*>(ws);
     hipError_t e = pss::launch_sparse_update(p, indices, offsets, grad_out,
                                              static_cast<char*>(ws) + 256, count, shared, bf16,
                                              state, lr, hash_params->eps, stream);
-    const hipError_t ef = hipFreeAsync(ws, stream);
+    const hipError_t ef = stream_scratch_done(ws, kept, stream);
     return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
   }
 
@@ -218,8 +274,9 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   const size_t g_bytes = fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
   const size_t ws_bytes = sorted ? pss::sorted_workspace_bytes(p) : 0;
   void* ws = nullptr;
+  bool kept = false;
   if (g_bytes + ws_bytes > 0) {
-    st = scratch_alloc(&ws, g_bytes + ws_bytes, stream);
+    st = stream_scratch(&ws, g_bytes + ws_bytes, stream, &kept);
     if (st != PSS_OK) return st;
   }
   float* dst = fused ? static_cast<float*>(shared) : static_cast<float*>(ws);
@@ -233,7 +290,7 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   }
   if (e == hipSuccess && !fused)
     e = pss::launch_optimizer(shared, bf16, state, dst, M, lr, hash_params->eps, stream);
-  const hipError_t ef = ws ? hipFreeAsync(ws, stream) : hipSuccess;
+  const hipError_t ef = stream_scratch_done(ws, kept, stream);
   if (e != hipSuccess || ef != hipSuccess) return PSS_ERR_HIP;
   return PSS_OK;
 }
@@ -251,8 +308,9 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
   if (capacity < sparse_capacity(M, p)) return PSS_ERR_INVALID_ARG;
   if (p.N > 0 && (locations == nullptr || values == nullptr)) return PSS_ERR_INVALID_ARG;
   void* ws = nullptr;
+  bool kept = false;
   const size_t ws_bytes = 256 + (p.N > 0 ? pss::sparse_workspace_bytes(p) : 0);
-  st = scratch_alloc(&ws, ws_bytes, stream);
+  st = stream_scratch(&ws, ws_bytes, stream, &kept);
   if (st != PSS_OK) return st;
   uint32_t* count = static_cast<uint32_t*>(ws);
   hipError_t e = hipSuccess;
@@ -263,7 +321,7 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
                                     locations, values, capacity, count, stream);
   }
   if (e == hipSuccess) e = pss::launch_store_count(count, num_unique, stream);
-  const hipError_t ef = hipFreeAsync(ws, stream);
+  const hipError_t ef = stream_scratch_done(ws, kept, stream);
   return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
 }
 
@@ -289,6 +347,23 @@ int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash
     return PSS_ERR_INVALID_ARG;
   const KParams p = make_params(M, Z, d, hash_params);
   return hip_status(pss::launch_debug_addresses(p, indices, offsets, nullptr, sign_out, stream));
+}
+
+int pss_release_scratch(void) {
+  std::lock_guard<std::mutex> lock(g_kept_mu);
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return PSS_ERR_HIP;
+  int status = PSS_OK;
+  for (auto& kv : g_kept) {
+    if (kv.second.ptr == nullptr) continue;
+    // the buffer may still be in use by work enqueued on its stream
+    if (hipSetDevice(kv.first.first) != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
+        hipFreeAsync(kv.second.ptr, nullptr) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+      status = PSS_ERR_HIP;
+  }
+  g_kept.clear();
+  if (hipSetDevice(cur) != hipSuccess) status = PSS_ERR_HIP;
+  return status;
 }
 
 int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N) {

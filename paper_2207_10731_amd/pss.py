@@ -72,9 +72,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_validate_offsets_host.argtypes = [vp, i64, i64]
     lib.pss_status_string.argtypes = [ctypes.c_int]
     lib.pss_status_string.restype = ctypes.c_char_p
+    lib.pss_release_scratch.argtypes = []
     for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
                  "pss_debug_addresses", "pss_debug_signs", "pss_gradient_sparse",
-                 "pss_hash_bases_host", "pss_hash_signs_host", "pss_validate_offsets_host"):
+                 "pss_hash_bases_host", "pss_hash_signs_host", "pss_validate_offsets_host",
+                 "pss_release_scratch"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -253,6 +255,11 @@ def pss_validate_offsets_host(offsets, num_bags, N) -> int:
     off = np.ascontiguousarray(offsets, dtype=np.int64)
     return load_library().pss_validate_offsets_host(off.ctypes.data_as(ctypes.c_void_p),
                                                     num_bags, N)
+
+
+def pss_release_scratch():
+    """Frees the scratch buffers the library keeps per (device, stream)."""
+    _check(load_library().pss_release_scratch(), "pss_release_scratch")
 
 
 def pss_status_string(status: int) -> str:

@@ -65,7 +65,8 @@
  *   preconditions that are not checked on the device; whatever they hold,
  *   every address the kernels touch stays inside the arrays described above
  *   (hash addresses are reduced mod M; item ranges are clamped to [0, N]).
- * Threads.  Concurrent calls on different streams are safe.
+ * Threads.  Concurrent calls on different streams are safe; calls made on one
+ *   stream from several threads at once are enqueued one after the other.
  */
 #ifndef PSS_H
 #define PSS_H

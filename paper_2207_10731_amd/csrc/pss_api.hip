@@ -142,55 +142,76 @@ int scratch_alloc(void** ptr, size_t bytes, hipStream_t stream) {
 // stream-ordered free per call cost the stream a marker between steps and
 // block the host until earlier frees have completed; a kept buffer costs
 // neither.  Work on one stream runs in order, so consecutive calls on it
-// may share the buffer.  Streams are told apart by handle: the runtime
-// keeps a stream object (whose address is the handle) alive while commands
-// enqueued on it are pending, so a handle is reused only after the work of
-// the stream it named has finished.
+// may share the buffer; a call holds the buffer's lock from taking it until
+// its work is enqueued, so that calls made on one stream from several host
+// threads do not interleave their kernels.  Streams are told apart by
+// handle: the runtime keeps a stream object (whose address is the handle)
+// alive while commands enqueued on it are pending, so a handle is reused
+// only after the work of the stream it named has finished.
 struct KeptScratch {
+  std::mutex mu;
   void* ptr = nullptr;
   size_t bytes = 0;
 };
-std::mutex g_kept_mu;
+std::mutex g_kept_mu;  // guards the map (std::map nodes do not move)
 std::map<std::pair<int, uintptr_t>, KeptScratch> g_kept;
 
-// Scratch of `bytes` for work enqueued on `stream`.  *kept says whether it
-// is a kept buffer (nothing to return) or a pool allocation that the caller
-// returns with hipFreeAsync on the stream after enqueueing its work: so it
-// is while the stream is being captured into a graph (the graph then owns
-// its allocation, and replays on other streams cannot share a kept buffer)
-// or when the capture status cannot be read.
-int stream_scratch(void** ptr, size_t bytes, hipStream_t stream, bool* kept) {
-  *kept = false;
-  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  int dev = 0;
-  if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone ||
-      hipGetDevice(&dev) != hipSuccess) {
-    (void)hipGetLastError();
-    return scratch_alloc(ptr, bytes, stream);
+// Scratch of one call for work enqueued on `stream`: a kept buffer, or a
+// pool allocation returned on the stream by done() (while the stream is
+// being captured into a graph, which then owns its allocation and whose
+// replays on other streams must not share a kept buffer, or when the
+// capture status cannot be read).
+class CallScratch {
+ public:
+  int take(size_t bytes, hipStream_t stream) {
+    stream_ = stream;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    int dev = 0;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone ||
+        hipGetDevice(&dev) != hipSuccess) {
+      (void)hipGetLastError();
+      const int st = scratch_alloc(&ptr_, bytes, stream);
+      if (st != PSS_OK) ptr_ = nullptr;
+      return st;
+    }
+    {
+      std::lock_guard<std::mutex> map_lock(g_kept_mu);
+      kept_ = &g_kept[{dev, reinterpret_cast<uintptr_t>(stream)}];
+    }
+    lock_ = std::unique_lock<std::mutex>(kept_->mu);
+    if (kept_->bytes < bytes) {
+      // the smaller buffer goes back to the pool after the work already
+      // enqueued on the stream
+      if (kept_->ptr != nullptr && hipFreeAsync(kept_->ptr, stream) != hipSuccess) return PSS_ERR_HIP;
+      kept_->ptr = nullptr;
+      kept_->bytes = 0;
+      const int st = scratch_alloc(&kept_->ptr, bytes, stream);
+      if (st != PSS_OK) {
+        kept_->ptr = nullptr;
+        return st;
+      }
+      kept_->bytes = bytes;
+    }
+    ptr_ = kept_->ptr;
+    return PSS_OK;
   }
-  std::lock_guard<std::mutex> lock(g_kept_mu);
-  KeptScratch& k = g_kept[{dev, reinterpret_cast<uintptr_t>(stream)}];
-  if (k.bytes < bytes) {
-    // the smaller buffer goes back to the pool after the work already
-    // enqueued on the stream
-    if (k.ptr != nullptr && hipFreeAsync(k.ptr, stream) != hipSuccess) return PSS_ERR_HIP;
-    k.ptr = nullptr;
-    k.bytes = 0;
-    void* p = nullptr;
-    const int st = scratch_alloc(&p, bytes, stream);
-    if (st != PSS_OK) return st;
-    k.ptr = p;
-    k.bytes = bytes;
+  void* ptr() const { return ptr_; }
+  // Call once the work using the scratch is enqueued.
+  hipError_t done() {
+    hipError_t e = hipSuccess;
+    if (kept_ == nullptr && ptr_ != nullptr) e = hipFreeAsync(ptr_, stream_);
+    ptr_ = nullptr;
+    if (lock_.owns_lock()) lock_.unlock();
+    return e;
   }
-  *ptr = k.ptr;
-  *kept = true;
-  return PSS_OK;
-}
+  ~CallScratch() { (void)done(); }
 
-// Returns scratch from stream_scratch: pool allocations go back on the stream.
-hipError_t stream_scratch_done(void* ptr, bool kept, hipStream_t stream) {
-  return (ptr == nullptr || kept) ? hipSuccess : hipFreeAsync(ptr, stream);
-}
+ private:
+  hipStream_t stream_ = nullptr;
+  void* ptr_ = nullptr;
+  KeptScratch* kept_ = nullptr;
+  std::unique_lock<std::mutex> lock_;
+};
 
 int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; }
 
@@ -254,15 +275,15 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
     // Alg. 1 sparse branch: unique locations + summed values, with the
     // optimizer applied at each location as it is summed.
     const size_t ws_bytes = pss::sparse_workspace_bytes(p);
-    void* ws = nullptr;
-    bool kept = false;
-    st = stream_scratch(&ws, 256 + ws_bytes, stream, &kept);
+    CallScratch scratch;
+    st = scratch.take(256 + ws_bytes, stream);
     if (st != PSS_OK) return st;
+    void* ws = scratch.ptr();
     uint32_t* count = static_cast<uint32_t*>(ws);
     hipError_t e = pss::launch_sparse_update(p, indices, offsets, grad_out,
                                              static_cast<char*>(ws) + 256, count, shared, bf16,
                                              state, lr, hash_params->eps, stream);
-    const hipError_t ef = stream_scratch_done(ws, kept, stream);
+    const hipError_t ef = scratch.done();
     return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
   }
 
@@ -273,12 +294,12 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   const bool fused = state == nullptr && !bf16;
   const size_t g_bytes = fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
   const size_t ws_bytes = sorted ? pss::sorted_workspace_bytes(p) : 0;
-  void* ws = nullptr;
-  bool kept = false;
+  CallScratch scratch;
   if (g_bytes + ws_bytes > 0) {
-    st = stream_scratch(&ws, g_bytes + ws_bytes, stream, &kept);
+    st = scratch.take(g_bytes + ws_bytes, stream);
     if (st != PSS_OK) return st;
   }
+  void* ws = scratch.ptr();
   float* dst = fused ? static_cast<float*>(shared) : static_cast<float*>(ws);
   void* sort_ws = static_cast<char*>(ws) + g_bytes;
   const float scale = fused ? -lr : 1.f;
@@ -290,7 +311,7 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   }
   if (e == hipSuccess && !fused)
     e = pss::launch_optimizer(shared, bf16, state, dst, M, lr, hash_params->eps, stream);
-  const hipError_t ef = stream_scratch_done(ws, kept, stream);
+  const hipError_t ef = scratch.done();
   if (e != hipSuccess || ef != hipSuccess) return PSS_ERR_HIP;
   return PSS_OK;
 }
@@ -307,11 +328,11 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
   if (p.N * static_cast<int64_t>(p.C) >= (1ll << 31)) return PSS_ERR_UNSUPPORTED;
   if (capacity < sparse_capacity(M, p)) return PSS_ERR_INVALID_ARG;
   if (p.N > 0 && (locations == nullptr || values == nullptr)) return PSS_ERR_INVALID_ARG;
-  void* ws = nullptr;
-  bool kept = false;
   const size_t ws_bytes = 256 + (p.N > 0 ? pss::sparse_workspace_bytes(p) : 0);
-  st = stream_scratch(&ws, ws_bytes, stream, &kept);
+  CallScratch scratch;
+  st = scratch.take(ws_bytes, stream);
   if (st != PSS_OK) return st;
+  void* ws = scratch.ptr();
   uint32_t* count = static_cast<uint32_t*>(ws);
   hipError_t e = hipSuccess;
   if (p.N == 0) {
@@ -321,7 +342,7 @@ int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
                                     locations, values, capacity, count, stream);
   }
   if (e == hipSuccess) e = pss::launch_store_count(count, num_unique, stream);
-  const hipError_t ef = stream_scratch_done(ws, kept, stream);
+  const hipError_t ef = scratch.done();
   return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
 }
 
@@ -355,6 +376,7 @@ int pss_release_scratch(void) {
   if (hipGetDevice(&cur) != hipSuccess) return PSS_ERR_HIP;
   int status = PSS_OK;
   for (auto& kv : g_kept) {
+    std::lock_guard<std::mutex> entry_lock(kv.second.mu);
     if (kv.second.ptr == nullptr) continue;
     // the buffer may still be in use by work enqueued on its stream
     if (hipSetDevice(kv.first.first) != hipSuccess || hipDeviceSynchronize() != hipSuccess ||

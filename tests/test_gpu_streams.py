@@ -103,3 +103,33 @@ def test_graph_capture_replays(variant):
         other.backward(g_other)
         _check(other, g_other)
     del graph
+
+
+def test_threads_on_one_stream():
+    """Four host threads enqueue backward calls on the same stream at once;
+    each call's kernels stay together in the stream, so the shared scratch
+    buffer is never used by two calls at a time."""
+    import threading
+    dev = torch.device("cuda", 0)
+    Ls = [Layer(synth.get("c2"), B=700, batch=k) for k in range(4)]
+    gs = [synth.make_grad(L.wl, B=L.B, batch=k) for k, L in enumerate(Ls)]
+    ds = [torch.from_numpy(g).to(dev) for g in gs]
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    errors = []
+
+    def work(k):
+        try:
+            _launch_backward(Ls[k], ds[k], stream)
+        except Exception as exc:  # surfaced below
+            errors.append(exc)
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for L, g in zip(Ls, gs):
+        _check(L, g)

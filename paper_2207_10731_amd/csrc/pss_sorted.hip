@@ -374,7 +374,8 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
 // phases separated by workgroup barriers (LDS-only fences: no wait for the
 // atomics); in phase k a reader fills buffer k mod 2 while its depositor
 // drains buffer (k-1) mod 2.  Rows of batch k+1 are requested before batch
-// k is summed.  A run crossing a quarter boundary deposits once per quarter.
+// k is summed.  A run crossing a quarter boundary leaves one partial sum per
+// quarter in LDS and is deposited once, after the last phase.
 constexpr int kPiece = 256;                 // pairs per workgroup
 constexpr int kReaders = kPiece / kWave;    // 4
 constexpr int kReduceThreads = 2 * kPiece;  // readers + depositors

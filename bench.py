@@ -2,7 +2,11 @@
 
 One step = pss_forward + pss_backward_update (forward gather/pool, backward
 deposit, optimizer step) over one batch of synthetic bags, rotating 4
-pre-generated index batches and gradient batches resident in HBM.
+pre-generated index batches and gradient batches resident in HBM.  The
+forward carries PSS_PREPARE_BACKWARD (as a training loop would): the
+backward's grouping of the batch runs on a library stream beside the
+forward kernel and the backward reuses it (--no-prepare: the backward
+groups the batch itself).
 
 Default workload: criteo-tb-shaped one-hot batch (26 tables with log-uniform
 cardinalities in [3, 4e7], Zipf(1.1) indices, batch 65536, d = 128, Z = 32,
@@ -139,6 +143,8 @@ def main():
     ap.add_argument("--config", default="c2")
     ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted", "sparse"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prepare", action="store_true",
+                    help="forward without PSS_PREPARE_BACKWARD")
     ap.add_argument("--event-every", type=int, default=5,
                     help="time the calls of every n-th timed step with HIP events")
     args = ap.parse_args()
@@ -174,6 +180,8 @@ def main():
     gen.manual_seed(wl.data_seed)
     grads = [torch.randn((wl.B, wl.T * wl.d), generator=gen, device=dev) for _ in range(ROTATE)]
     out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=dev)
+    if not args.no_prepare:
+        flags |= pss.PSS_PREPARE_BACKWARD
     hps = [pss.make_hash_params(wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=x.N,
                                 weight_dtype=dt_code, eps=wl.eps, flags=flags) for x in xs]
     torch.cuda.synchronize()
@@ -251,7 +259,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "tables": wl.T, "batch": wl.B, "d": wl.d, "Z": wl.Z,
                    "M": wl.M, "storage": wl.weight_dtype, "optimizer": wl.optimizer,
-                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant,
+                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": not args.no_prepare,
                    "lookups_per_step": N_avg},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,

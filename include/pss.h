@@ -43,6 +43,17 @@
  *   PSS_INDEX_I32  indices and offsets are int32.
  *   PSS_ROWS_BF16  out is written, and grad_out read, as bfloat16 (out is
  *     rounded to nearest even from the float32 result).
+ *   PSS_PREPARE_BACKWARD  read by pss_forward only (the other calls ignore
+ *     it): the forward also groups the batch's lookups by token for the
+ *     backward, on a library-owned stream that runs beside the forward
+ *     kernel.  The next pss_backward_update on the same stream uses that
+ *     grouping when its indices and offsets pointers, batch shape, hash
+ *     parameters and options match and it runs the SORTED variant (AUTO's
+ *     choice for SGD on float32 storage); it drops the grouping either way.
+ *     The caller must not change the contents of indices or offsets between
+ *     the two calls.  Ignored while the stream is being captured into a
+ *     graph, and for an explicit ATOMIC or SPARSE variant.  Holds one
+ *     buffer of 16 B per lookup per stream (see "Memory").
  * Shared array.  `shared` holds M elements of the storage type named by
  *   pss_hash_params.weight_dtype (float32, or bfloat16 bit patterns).
  *   Arithmetic is float32 throughout; bfloat16 values are widened exactly on
@@ -52,7 +63,9 @@
  *   enqueued.  Scratch space of the backward and sparse-gradient calls is a
  *   library-owned device buffer kept per (device, stream) between calls and
  *   grown to the largest call made on that stream (taken from a
- *   library-owned memory pool); pss_release_scratch returns these buffers.
+ *   library-owned memory pool), and so does a forward call with
+ *   PSS_PREPARE_BACKWARD, together with a library stream and two events;
+ *   pss_release_scratch returns all of these.
  *   While `stream` is being captured into a graph, scratch is allocated
  *   stream-ordered from the pool and freed on the same stream instead, so
  *   that the graph owns it.
@@ -112,14 +125,15 @@ enum {
 enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2, PSS_BWD_SPARSE = 3 };
 #define PSS_BWD_MASK 3u
 
-/* Options, bits 2-6 of pss_hash_params.flags (see "Options" above). */
+/* Options, bits 2-7 of pss_hash_params.flags (see "Options" above). */
 #define PSS_SIGN_PM1 (1u << 2)
 #define PSS_SIGN_SPARSE (2u << 2)
 #define PSS_SIGN_MASK (3u << 2)
 #define PSS_POOL_MEAN (1u << 4)
 #define PSS_INDEX_I32 (1u << 5)
 #define PSS_ROWS_BF16 (1u << 6)
-#define PSS_FLAGS_ALL 0x7fu
+#define PSS_PREPARE_BACKWARD (1u << 7)
+#define PSS_FLAGS_ALL 0xffu
 
 typedef struct {
   uint32_t a;            /* hash multiplier, 1 <= a <= p - 1 */
@@ -228,11 +242,12 @@ int pss_hash_signs_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
 int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N);
 
 /* Static, NUL-terminated description of a status code. */
-/* Frees the scratch buffers kept between calls (see "Memory" above) on
- * every device that holds one, after waiting for that device's work to
- * finish.  Host only; no call of this library may be in progress on another
- * thread.  Later calls allocate afresh.  Returns PSS_ERR_HIP if a runtime
- * call fails (the buffers are forgotten either way). */
+/* Frees the scratch buffers kept between calls, and the streams, events and
+ * buffers of PSS_PREPARE_BACKWARD (see "Memory" above), on every device that
+ * holds them, after waiting for that device's work to finish.  Host only; no
+ * call of this library may be in progress on another thread.  Later calls
+ * allocate afresh; a prepared grouping not yet used is dropped.  Returns
+ * PSS_ERR_HIP if a runtime call fails (everything is forgotten either way). */
 int pss_release_scratch(void);
 
 const char* pss_status_string(int status);

@@ -213,6 +213,119 @@ class CallScratch {
   std::unique_lock<std::mutex> lock_;
 };
 
+// Grouping prepared by a forward call with PSS_PREPARE_BACKWARD, one slot
+// per (device, caller stream).  The grouping runs on a library stream of its
+// own, after the caller's stream has reached the forward call (event
+// `start`), so it overlaps the forward kernel; `ready` marks its end.  The
+// next backward on the caller's stream with the same indices, offsets and
+// grouping parameters waits for `ready` and reuses the pairs instead of
+// grouping again.  A later prepare on the same stream reuses the buffer: its
+// grouping waits for `start`, recorded after every earlier call on the
+// caller's stream (including the backward that read the buffer).
+struct Prepared {
+  std::mutex mu;
+  hipStream_t side = nullptr;
+  hipEvent_t start = nullptr;
+  hipEvent_t ready = nullptr;
+  void* buf = nullptr;
+  size_t bytes = 0;
+  bool valid = false;  // a grouping waits for its backward
+  const void* indices = nullptr;
+  const void* offsets = nullptr;
+  KParams made{};
+  pss::GroupedPairs pairs;
+};
+std::mutex g_prep_mu;  // guards the map (std::map nodes do not move)
+std::map<std::pair<int, uintptr_t>, Prepared> g_prep;
+
+// Parameters the grouping depends on.
+bool same_grouping(const KParams& x, const KParams& y) {
+  return x.N == y.N && x.num_bags == y.num_bags && x.T == y.T && x.B == y.B && x.C == y.C &&
+         x.a == y.a && x.b == y.b && x.mean == y.mean && x.idx32 == y.idx32;
+}
+
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return true;  // unknown: treat as captured (no side stream)
+  }
+  return cs != hipStreamCaptureStatusNone;
+}
+
+int prepare_backward(const KParams& p, const void* indices, const void* offsets,
+                     hipStream_t stream) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return PSS_ERR_HIP;
+  Prepared* pr = nullptr;
+  {
+    std::lock_guard<std::mutex> map_lock(g_prep_mu);
+    pr = &g_prep[{dev, reinterpret_cast<uintptr_t>(stream)}];
+  }
+  std::lock_guard<std::mutex> lock(pr->mu);
+  pr->valid = false;
+  if (pr->side == nullptr) {
+    if (hipStreamCreateWithFlags(&pr->side, hipStreamNonBlocking) != hipSuccess) {
+      pr->side = nullptr;
+      return PSS_ERR_HIP;
+    }
+    if (hipEventCreateWithFlags(&pr->start, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&pr->ready, hipEventDisableTiming) != hipSuccess)
+      return PSS_ERR_HIP;
+  }
+  if (hipEventRecord(pr->start, stream) != hipSuccess ||
+      hipStreamWaitEvent(pr->side, pr->start, 0) != hipSuccess)
+    return PSS_ERR_HIP;
+  const size_t need = pss::sorted_workspace_bytes(p);
+  if (pr->bytes < need) {
+    // both stream-ordered on the library stream, after the caller's earlier work
+    if (pr->buf != nullptr && hipFreeAsync(pr->buf, pr->side) != hipSuccess) return PSS_ERR_HIP;
+    pr->buf = nullptr;
+    pr->bytes = 0;
+    const int st = scratch_alloc(&pr->buf, need, pr->side);
+    if (st != PSS_OK) {
+      pr->buf = nullptr;
+      return st;
+    }
+    pr->bytes = need;
+  }
+  if (pss::launch_group_sorted(p, indices, offsets, pr->buf, pr->side, &pr->pairs) != hipSuccess ||
+      hipEventRecord(pr->ready, pr->side) != hipSuccess)
+    return PSS_ERR_HIP;
+  pr->indices = indices;
+  pr->offsets = offsets;
+  pr->made = p;
+  pr->valid = true;
+  return PSS_OK;
+}
+
+// The grouping prepared by the last forward on `stream`, if it was made for
+// this batch and `usable`; nullptr otherwise.  A prepared grouping serves the
+// next backward call on its stream only: this call drops it either way.  On
+// success *lock holds the slot until the caller's work is enqueued.
+Prepared* take_prepared(hipStream_t stream, const void* indices, const void* offsets,
+                        const KParams& p, bool usable, std::unique_lock<std::mutex>* lock) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  Prepared* pr = nullptr;
+  {
+    std::lock_guard<std::mutex> map_lock(g_prep_mu);
+    auto it = g_prep.find({dev, reinterpret_cast<uintptr_t>(stream)});
+    if (it == g_prep.end()) return nullptr;
+    pr = &it->second;
+  }
+  std::unique_lock<std::mutex> slot(pr->mu);
+  const bool match = pr->valid && pr->indices == indices && pr->offsets == offsets &&
+                     same_grouping(pr->made, p);
+  pr->valid = false;
+  if (!match || !usable) return nullptr;
+  *lock = std::move(slot);
+  return pr;
+}
+
 int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; }
 
 uint64_t splitmix64_next(uint64_t* state) {
@@ -248,6 +361,14 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
   if (shared == nullptr || offsets == nullptr || out == nullptr) return PSS_ERR_INVALID_ARG;
   if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
   const KParams p = make_params(M, Z, d, hash_params);
+  // The grouping is only reused by the SORTED backward (AUTO's choice when
+  // the update is fused), and only outside graph capture.
+  const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
+  if ((hash_params->flags & PSS_PREPARE_BACKWARD) && p.N > 0 &&
+      (variant == PSS_BWD_AUTO || variant == PSS_BWD_SORTED) && !capturing(stream)) {
+    const int pst = prepare_backward(p, indices, offsets, stream);
+    if (pst != PSS_OK) return pst;
+  }
   return hip_status(pss::launch_forward(shared, hash_params->weight_dtype == PSS_BF16, p, indices,
                                         offsets, out, stream));
 }
@@ -270,6 +391,9 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (variant == PSS_BWD_SPARSE && !sparse_fits) return PSS_ERR_UNSUPPORTED;
   if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
   if (variant == PSS_BWD_AUTO) variant = auto_variant(M, p, state != nullptr || bf16, sparse_fits);
+  std::unique_lock<std::mutex> prep_lock;
+  Prepared* prep = take_prepared(stream, indices, offsets, p,
+                                 variant == PSS_BWD_SORTED && !capturing(stream), &prep_lock);
 
   if (variant == PSS_BWD_SPARSE) {
     // Alg. 1 sparse branch: unique locations + summed values, with the
@@ -293,7 +417,7 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   // the shared array.  Otherwise deposit G into a scratch buffer first.
   const bool fused = state == nullptr && !bf16;
   const size_t g_bytes = fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
-  const size_t ws_bytes = sorted ? pss::sorted_workspace_bytes(p) : 0;
+  const size_t ws_bytes = (sorted && prep == nullptr) ? pss::sorted_workspace_bytes(p) : 0;
   CallScratch scratch;
   if (g_bytes + ws_bytes > 0) {
     st = scratch.take(g_bytes + ws_bytes, stream);
@@ -305,7 +429,11 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   const float scale = fused ? -lr : 1.f;
   hipError_t e = hipSuccess;
   if (!fused) e = pss::launch_zero(dst, M, stream);
-  if (e == hipSuccess) {
+  if (e == hipSuccess && prep != nullptr) {
+    // the grouping ran on the library stream during the forward
+    e = hipStreamWaitEvent(stream, prep->ready, 0);
+    if (e == hipSuccess) e = pss::launch_reduce_sorted(dst, scale, p, prep->pairs, grad_out, stream);
+  } else if (e == hipSuccess) {
     e = sorted ? pss::launch_deposit_sorted(dst, scale, p, indices, offsets, grad_out, sort_ws, stream)
                : pss::launch_deposit_atomic(dst, scale, p, indices, offsets, grad_out, stream);
   }
@@ -384,6 +512,22 @@ int pss_release_scratch(void) {
       status = PSS_ERR_HIP;
   }
   g_kept.clear();
+  {
+    std::lock_guard<std::mutex> map_lock(g_prep_mu);
+    for (auto& kv : g_prep) {
+      Prepared& pr = kv.second;
+      std::lock_guard<std::mutex> entry_lock(pr.mu);
+      if (hipSetDevice(kv.first.first) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+        status = PSS_ERR_HIP;
+      if (pr.buf != nullptr && (hipFreeAsync(pr.buf, nullptr) != hipSuccess ||
+                                hipDeviceSynchronize() != hipSuccess))
+        status = PSS_ERR_HIP;
+      if (pr.start != nullptr && hipEventDestroy(pr.start) != hipSuccess) status = PSS_ERR_HIP;
+      if (pr.ready != nullptr && hipEventDestroy(pr.ready) != hipSuccess) status = PSS_ERR_HIP;
+      if (pr.side != nullptr && hipStreamDestroy(pr.side) != hipSuccess) status = PSS_ERR_HIP;
+    }
+    g_prep.clear();
+  }
   if (hipSetDevice(cur) != hipSuccess) status = PSS_ERR_HIP;
   return status;
 }

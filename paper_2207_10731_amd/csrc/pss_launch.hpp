@@ -26,6 +26,18 @@ size_t sorted_workspace_bytes(const KParams& p);
 hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,
                                  const void* offsets, const void* grad, void* workspace,
                                  hipStream_t stream);
+// Its two halves.  The grouping depends on the indices, offsets and hash
+// parameters only (not on grad or the shared array), so it may run ahead on
+// another stream; it leaves the grouped pairs inside `workspace`.
+struct GroupedPairs {
+  const uint32_t* keys = nullptr;  // item hash h0 of each lookup, grouped
+  const uint32_t* rows = nullptr;  // its pooled row b*T + t
+  const float* inv_len = nullptr;  // 1 / |bag| per pooled row (mean pooling)
+};
+hipError_t launch_group_sorted(const KParams& p, const void* indices, const void* offsets,
+                               void* workspace, hipStream_t stream, GroupedPairs* out);
+hipError_t launch_reduce_sorted(float* dst, float scale, const KParams& p, const GroupedPairs& g,
+                                const void* grad, hipStream_t stream);
 
 // Building blocks of the sorted path, shared with the sparse-gradient path.
 // keygen: keys[e] = item part of the hash of lookup e, rows[e] = b*T + t;

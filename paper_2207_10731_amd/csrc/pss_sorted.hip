@@ -740,11 +740,9 @@ static hipError_t launch_reduce_g(float* dst, float scale, const KParams& p, con
   return launch_reduce_s<false>(dst, scale, p, keys, rows, grad, il, stream);
 }
 
-hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,
-                                 const void* offsets, const void* grad, void* workspace,
-                                 hipStream_t stream) {
+hipError_t launch_group_sorted(const KParams& p, const void* indices, const void* offsets,
+                               void* workspace, hipStream_t stream, GroupedPairs* out) {
   const int64_t N = p.N;
-  if (N == 0) return hipSuccess;
   uint32_t* k0 = static_cast<uint32_t*>(workspace);
   uint32_t* v0 = k0 + N;
   uint32_t* k1 = v0 + N;
@@ -753,6 +751,10 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   float* inv_len = p.mean ? reinterpret_cast<float*>(
                                 reinterpret_cast<char*>(scratch) + radix_scratch_bytes(N))
                           : nullptr;
+  out->keys = k0;
+  out->rows = v0;
+  out->inv_len = inv_len;
+  if (N == 0) return hipSuccess;
   // As many items as bags (one-hot batches): keygen in item space, fused
   // with the first pass's histogram.
   const bool item_space = static_cast<uint64_t>(N) == p.num_bags;
@@ -771,11 +773,28 @@ hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, cons
   }
   if (e == hipSuccess)
     e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), scratch, stream, nullptr, item_space);
-  if (e != hipSuccess) return e;
+  out->keys = k0;
+  out->rows = v0;
+  return e;
+}
+
+hipError_t launch_reduce_sorted(float* dst, float scale, const KParams& p, const GroupedPairs& g,
+                                const void* grad, hipStream_t stream) {
+  if (p.N == 0) return hipSuccess;
   if (p.rows_bf16)
-    return launch_reduce_g(dst, scale, p, k0, v0, static_cast<const uint16_t*>(grad), inv_len,
-                           stream);
-  return launch_reduce_g(dst, scale, p, k0, v0, static_cast<const float*>(grad), inv_len, stream);
+    return launch_reduce_g(dst, scale, p, g.keys, g.rows, static_cast<const uint16_t*>(grad),
+                           g.inv_len, stream);
+  return launch_reduce_g(dst, scale, p, g.keys, g.rows, static_cast<const float*>(grad), g.inv_len,
+                         stream);
+}
+
+hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,
+                                 const void* offsets, const void* grad, void* workspace,
+                                 hipStream_t stream) {
+  GroupedPairs g;
+  const hipError_t e = launch_group_sorted(p, indices, offsets, workspace, stream, &g);
+  if (e != hipSuccess) return e;
+  return launch_reduce_sorted(dst, scale, p, g, grad, stream);
 }
 
 }  // namespace pss

@@ -141,7 +141,7 @@ def _bad_call(lib, **kw):
 
 @pytest.mark.parametrize("kw", [dict(M=0), dict(M=2**31), dict(Z=0), dict(Z=5000, M=4096),
                                 dict(Z=3), dict(d=4097 * 4), dict(a=0), dict(a=P),
-                                dict(b=P), dict(T=0), dict(B=0), dict(N=-1), dict(flags=1 << 7),
+                                dict(b=P), dict(T=0), dict(B=0), dict(N=-1), dict(flags=1 << 8),
                                 dict(flags=3 << 2), dict(flags=pss.PSS_SIGN_PM1, sign_a=0),
                                 dict(flags=pss.PSS_SIGN_SPARSE, sign_a=P),
                                 dict(flags=pss.PSS_SIGN_PM1, sign_b=P),
@@ -166,7 +166,7 @@ def test_backward_rejects_bad_arguments(lib):
     hp_neg = pss.pss_hash_params(5, 7, 4, 2, 8, 0, -1.0, 0)
     assert f(dummy, dummy, 4096, 4, 16, ctypes.byref(hp_neg), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
-    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 1 << 7)
+    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 1 << 8)
     assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp4), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
 

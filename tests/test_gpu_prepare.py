@@ -1,0 +1,153 @@
+"""PSS_PREPARE_BACKWARD: the forward groups the batch on a library stream for
+the next backward on the same stream.  Every result is checked against the
+oracle, including the cases where the prepared grouping must not be used."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from paper_2207_10731_amd import pss
+import parity
+from parity import Layer
+
+pytestmark = pytest.mark.gpu
+
+PREP = pss.PSS_PREPARE_BACKWARD
+
+
+def _check_forward(L, got):
+    ref, s_abs = L.ref_forward()
+    parity.check_forward(got, ref, s_abs, parity.RTOL[L.wl.weight_dtype])
+
+
+def _check_update(L, g):
+    w_ref, s_ref, G, A, _ = L.ref_backward(g)
+    s_gpu = None if L.state is None else L.state.cpu().numpy()
+    parity.check_update(L, L.weights(), s_gpu, w_ref, s_ref, G, A, L.wl.lr)
+
+
+@pytest.mark.parametrize("key,B,kw", [("c2", 700, {}), ("c2", 300, dict(idx32=True)),
+                                      ("c3", 50, dict(mean=True)), ("c1", None, {})],
+                         ids=["onehot", "onehot-i32", "multihot-mean", "tiny"])
+def test_prepared_step(key, B, kw):
+    L = Layer(synth.get(key), B=B, flags=pss.PSS_BWD_SORTED | PREP, **kw)
+    g = synth.make_grad(L.wl, B=L.B)
+    _check_forward(L, L.forward())
+    L.backward(g)
+    _check_update(L, g)
+
+
+def test_prepared_for_other_indices_is_not_used():
+    """Prepared for batch A, then a backward of batch B (same shapes) on the
+    same stream, then a backward of A: both are computed from their own
+    indices."""
+    A = Layer(synth.get("c2"), B=700, batch=0, flags=PREP)
+    Bl = Layer(synth.get("c2"), B=700, batch=1, flags=PREP)
+    gA = synth.make_grad(A.wl, B=A.B, batch=0)
+    gB = synth.make_grad(Bl.wl, B=Bl.B, batch=1)
+    A.forward()
+    Bl.backward(gB)
+    _check_update(Bl, gB)
+    A.backward(gA)
+    _check_update(A, gA)
+
+
+def test_two_forwards_then_two_backwards():
+    """Only the last forward's grouping is kept: the first backward groups
+    its batch itself, the second reuses the prepared one."""
+    A = Layer(synth.get("c2"), B=700, batch=0, flags=PREP)
+    Bl = Layer(synth.get("c2"), B=700, batch=1, flags=PREP)
+    gA = synth.make_grad(A.wl, B=A.B, batch=0)
+    gB = synth.make_grad(Bl.wl, B=Bl.B, batch=1)
+    A.forward()
+    Bl.forward()
+    A.backward(gA)
+    Bl.backward(gB)
+    _check_update(A, gA)
+    _check_update(Bl, gB)
+
+
+def test_repeated_steps_reuse_the_buffer():
+    """Several prepared steps in a row on one stream (weights updated in
+    place each step), against the oracle applied step by step."""
+    L = Layer(synth.get("c2"), B=400, flags=PREP)
+    w = L.w_host.copy()
+    for k in range(3):
+        g = synth.make_grad(L.wl, B=L.B, batch=k)
+        L.w_host = w
+        L.shared.copy_(torch.from_numpy(w).to(L.dev))
+        torch.cuda.synchronize()
+        L.forward()
+        L.backward(g)
+        _check_update(L, g)
+        w = L.weights().copy()
+
+
+def test_prepare_then_release():
+    L = Layer(synth.get("c2"), B=300, flags=PREP)
+    g = synth.make_grad(L.wl, B=L.B)
+    L.forward()
+    pss.pss_release_scratch()
+    L.backward(g)
+    _check_update(L, g)
+
+
+def test_prepared_step_in_a_graph():
+    """Forward with the flag and backward captured into one graph: under
+    capture the flag is ignored; three replays from the same weights, with
+    eager prepared steps in between, each match the oracle."""
+    dev = torch.device("cuda", 0)
+    L = Layer(synth.get("c2"), B=300, flags=PREP)
+    other = Layer(synth.get("c2"), B=500, batch=1, flags=PREP)
+    g = synth.make_grad(L.wl, B=L.B)
+    g_other = synth.make_grad(other.wl, B=other.B, batch=1)
+    g_dev = torch.from_numpy(g).to(dev)
+    w0 = torch.from_numpy(L.w_host).to(dev)
+    out = torch.empty((L.B, L.wl.T * L.wl.d), device=dev)
+    wl = L.wl
+    L.forward()
+    L.backward(g)  # eager warm-up outside capture
+    L.shared.copy_(w0)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        s = torch.cuda.current_stream()
+        pss.pss_forward(L.shared, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, out, stream=s)
+        pss.pss_backward_update(L.shared, None, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets,
+                                g_dev, wl.lr, stream=s)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        L.shared.copy_(w0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        _check_update(L, g)
+        got = out.cpu().numpy()
+        ref, s_abs = L.ref_forward()
+        parity.check_forward(got, ref, s_abs, parity.RTOL[wl.weight_dtype])
+        other.shared.copy_(torch.from_numpy(other.w_host).to(dev))
+        other.forward()
+        other.backward(g_other)
+        _check_update(other, g_other)
+    del graph
+    assert np.isfinite(L.weights()).all()
+
+
+def test_backward_uses_the_grouping_made_by_the_forward():
+    """White box: after the forward with the flag (and a synchronisation, so
+    its grouping has finished), the indices tensor is overwritten in place
+    with another batch's, which the flag forbids.  The backward still
+    deposits at the addresses of the batch the forward grouped: it used the
+    prepared grouping.  Without the flag the same sequence follows the new
+    contents."""
+    for flags, grouped_batch in [(PREP, 0), (0, 1)]:
+        L = Layer(synth.get("c2"), B=700, batch=0, flags=flags)
+        other = synth.make_inputs(L.wl, B=L.B, batch=1)
+        g = synth.make_grad(L.wl, B=L.B)
+        L.forward()
+        L.indices.copy_(torch.from_numpy(other.indices).to(L.dev))
+        torch.cuda.synchronize()
+        L.backward(g)
+        if grouped_batch == 1:
+            L.x = other
+        _check_update(L, g)

@@ -1,9 +1,10 @@
 """Full-size parity: every workload at its real size, through the same entry
 points and launch configuration that bench.py times (default backward
-variant), checked on sampled outputs the oracle evaluates one by one:
-pooled rows of sampled bags (forward_at) and updated weights at sampled
-elements of the shared array (gradient_at), half of them elements that the
-batch reads."""
+variant; the step as the bench runs it, with PSS_PREPARE_BACKWARD on the
+forward, for the one-hot and multi-hot workloads), checked on sampled
+outputs the oracle evaluates one by one: pooled rows of sampled bags
+(forward_at) and updated weights at sampled elements of the shared array
+(gradient_at), half of them elements that the batch reads."""
 import numpy as np
 import pytest
 import torch
@@ -19,7 +20,7 @@ RTOL = {"f32": 1e-5, "bf16": 1e-2}
 
 
 class Full:
-    def __init__(self, key):
+    def __init__(self, key, flags=0):
         print(f"full-size {key}: preparing inputs", flush=True)
         self.wl = wl = synth.get(key)
         self.x = synth.make_inputs(wl)
@@ -34,7 +35,7 @@ class Full:
         self.off = torch.from_numpy(self.x.offsets).to(self.dev)
         self.hp = pss.make_hash_params(
             wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=self.x.N, eps=wl.eps,
-            weight_dtype=pss.PSS_BF16 if wl.weight_dtype == "bf16" else pss.PSS_F32)
+            weight_dtype=pss.PSS_BF16 if wl.weight_dtype == "bf16" else pss.PSS_F32, flags=flags)
         self.a, self.b = self.hp.a, self.hp.b
 
 
@@ -46,6 +47,11 @@ def test_fullsize_forward_sampled_bags(key):
     print(f"full-size {key}: forward over {F.x.N} lookups", flush=True)
     pss.pss_forward(F.shared, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, out)
     torch.cuda.synchronize()
+    _check_forward(F, out)
+
+
+def _check_forward(F, out):
+    wl = F.wl
     rng = np.random.default_rng(100)
     nb = wl.T * wl.B
     bags = np.unique(np.concatenate([rng.choice(nb, 300, replace=False),
@@ -70,26 +76,54 @@ def _sample_elements(F, rng, n_read=1500, n_any=500):
     return np.unique(np.concatenate([read, anyw, [0, wl.M - 1]]))
 
 
+def _grad(F):
+    """N(0, 1) output gradient drawn on the device (seeded), and its host
+    copy for the oracle."""
+    wl = F.wl
+    gen = torch.Generator(device=F.dev).manual_seed(wl.data_seed)
+    g = torch.randn((wl.B, wl.T * wl.d), device=F.dev, generator=gen)
+    return g, g.cpu().numpy()
+
+
 @pytest.mark.parametrize("key", FULL)
 def test_fullsize_backward_sampled_elements(key):
     F = Full(key)
     wl = F.wl
-    # N(0, 1) output gradient drawn on the device (seeded), copied to the
-    # host for the oracle
-    gen = torch.Generator(device=F.dev).manual_seed(wl.data_seed)
-    g = torch.randn((wl.B, wl.T * wl.d), device=F.dev, generator=gen)
-    grad = g.cpu().numpy()
+    g, grad = _grad(F)
     print(f"full-size {key}: backward over {F.x.N} lookups", flush=True)
     pss.pss_backward_update(F.shared, F.state, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, wl.lr)
     torch.cuda.synchronize()
     del g
+    _check_backward(F, grad)
+
+
+@pytest.mark.parametrize("key", ["c2", "c3"])
+def test_fullsize_prepared_step(key):
+    """The bench's step: forward with PSS_PREPARE_BACKWARD (the grouping runs
+    beside the forward kernel), then the backward reusing it."""
+    F = Full(key, flags=pss.PSS_PREPARE_BACKWARD)
+    wl = F.wl
+    g, grad = _grad(F)
+    out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=F.dev)
+    torch.cuda.synchronize()
+    print(f"full-size {key}: prepared step over {F.x.N} lookups", flush=True)
+    pss.pss_forward(F.shared, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, out)
+    pss.pss_backward_update(F.shared, F.state, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, wl.lr)
+    torch.cuda.synchronize()
+    del g
+    _check_forward(F, out)
+    _check_backward(F, grad)
+
+
+def _check_backward(F, grad):
+    wl = F.wl
     where = _sample_elements(F, np.random.default_rng(200))
     wh = torch.from_numpy(where).to(F.dev)
     if wl.weight_dtype == "bf16":
         w_gpu = F.shared.view(torch.int16)[wh].cpu().numpy().view(np.uint16)
     else:
         w_gpu = F.shared[wh].cpu().numpy()
-    print(f"full-size {key}: oracle at {where.shape[0]} elements", flush=True)
+    print(f"full-size {wl.name}: oracle at {where.shape[0]} elements", flush=True)
     G, A, cnt = o.gradient_at(wl.M, wl.Z, wl.d, wl.T, wl.B, F.a, F.b, F.x.indices, F.x.offsets,
                               grad, where)
     assert (cnt > 0).sum() >= where.shape[0] // 2  # the read elements were sampled

@@ -264,14 +264,16 @@ int prepare_backward(const KParams& p, const void* indices, const void* offsets,
   }
   std::lock_guard<std::mutex> lock(pr->mu);
   pr->valid = false;
-  if (pr->side == nullptr) {
-    if (hipStreamCreateWithFlags(&pr->side, hipStreamNonBlocking) != hipSuccess) {
-      pr->side = nullptr;
+  // created on first use (each one again if an earlier creation failed)
+  if (pr->side == nullptr && hipStreamCreateWithFlags(&pr->side, hipStreamNonBlocking) != hipSuccess) {
+    pr->side = nullptr;
+    return PSS_ERR_HIP;
+  }
+  for (hipEvent_t* ev : {&pr->start, &pr->ready}) {
+    if (*ev == nullptr && hipEventCreateWithFlags(ev, hipEventDisableTiming) != hipSuccess) {
+      *ev = nullptr;
       return PSS_ERR_HIP;
     }
-    if (hipEventCreateWithFlags(&pr->start, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&pr->ready, hipEventDisableTiming) != hipSuccess)
-      return PSS_ERR_HIP;
   }
   if (hipEventRecord(pr->start, stream) != hipSuccess ||
       hipStreamWaitEvent(pr->side, pr->start, 0) != hipSuccess)

@@ -52,8 +52,9 @@
  *     choice for SGD on float32 storage); it drops the grouping either way.
  *     The caller must not change the contents of indices or offsets between
  *     the two calls.  Ignored while the stream is being captured into a
- *     graph, and for an explicit ATOMIC or SPARSE variant.  Holds one
- *     buffer of 16 B per lookup per stream (see "Memory").
+ *     graph, and for an explicit ATOMIC or SPARSE variant; if the grouping
+ *     cannot be set up (no memory for its buffer), the forward runs without
+ *     it.  Holds one buffer of 16 B per lookup per stream (see "Memory").
  * Shared array.  `shared` holds M elements of the storage type named by
  *   pss_hash_params.weight_dtype (float32, or bfloat16 bit patterns).
  *   Arithmetic is float32 throughout; bfloat16 values are widened exactly on

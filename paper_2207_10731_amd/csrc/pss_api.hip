@@ -366,10 +366,12 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
   // The grouping is only reused by the SORTED backward (AUTO's choice when
   // the update is fused), and only outside graph capture.
   const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
+  // The preparation only saves the backward some work: if it cannot be set
+  // up (no memory for its buffer, a failed runtime call), the forward runs
+  // anyway and the backward groups the batch itself.
   if ((hash_params->flags & PSS_PREPARE_BACKWARD) && p.N > 0 &&
       (variant == PSS_BWD_AUTO || variant == PSS_BWD_SORTED) && !capturing(stream)) {
-    const int pst = prepare_backward(p, indices, offsets, stream);
-    if (pst != PSS_OK) return pst;
+    if (prepare_backward(p, indices, offsets, stream) != PSS_OK) (void)hipGetLastError();
   }
   return hip_status(pss::launch_forward(shared, hash_params->weight_dtype == PSS_BF16, p, indices,
                                         offsets, out, stream));

@@ -21,6 +21,14 @@
 
 namespace pss {
 
+constexpr uint64_t kXcds = 8;  // XCDs of an MI355X
+// Shared arrays larger than the chip's aggregate L2 (8 x 4 MiB) get their
+// tiles partitioned over the XCDs (see forward_kernel).  Measured: the
+// multi-hot forward on a 64 MB array 1053 -> 867 us, the row-hash forward
+// on a 128 MB array 852 -> 832 us; on a 10 MB array the split is neutral
+// alone and slower beside a concurrent backward grouping.
+constexpr uint64_t kXcdSplitBytes = 32ull << 20;
+
 __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   const uint32_t lo = readlane_u32(static_cast<uint32_t>(v), lane);
   const uint32_t hi = readlane_u32(static_cast<uint32_t>(v >> 32), lane);
@@ -94,9 +102,18 @@ __device__ __forceinline__ void forward_onehot_tile(
 template <typename WT, int EPL, int U, bool TAB, bool SIGN>
 __global__ __launch_bounds__(kBlockThreads) void forward_kernel(
     const WT* __restrict__ w, const KParams p, const void* __restrict__ indices,
-    const void* __restrict__ offsets, void* __restrict__ out) {
+    const void* __restrict__ offsets, void* __restrict__ out, const uint32_t xcd_split) {
   const int lane = threadIdx.x & (kWave - 1);
-  const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+  // Workgroups are dispatched round-robin over the chip's XCDs (workgroup b
+  // on XCD b mod kXcds), each with an L2 of its own.  Tiles are table-major,
+  // so with xcd_split XCD x takes a contiguous share of the tiles and its L2
+  // holds the hot tokens of about 1/kXcds of the tables (grid.x is then a
+  // multiple of kXcds; any other dispatch order only changes which L2 sees
+  // which tile).
+  const uint64_t per_xcd = gridDim.x / kXcds;
+  const uint64_t blk =
+      xcd_split ? (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds : blockIdx.x;
+  const uint64_t wave = blk * kWavesPerBlock + (threadIdx.x >> 6);
   const uint64_t g0 = wave * kTileBags;
   if (g0 >= p.num_bags) return;
   const uint32_t c0 = blockIdx.y * (kWave * EPL);
@@ -213,10 +230,14 @@ static hipError_t launch_fwd_t(const WT* w, const KParams& p, const void* indice
   const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
   const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
-  if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
-  dim3 grid(static_cast<uint32_t>(blocks), slabs);
+  if (blocks > 0x7fffffffull - kXcds) return hipErrorInvalidConfiguration;
+  const uint32_t xcd_split = static_cast<uint64_t>(p.M) * sizeof(WT) > kXcdSplitBytes ? 1u : 0u;
+  // with the split, grid.x is rounded up to a multiple of kXcds (the extra
+  // workgroups' tiles lie past the last bag: they exit at once)
+  const uint64_t grid_x = xcd_split ? (blocks + kXcds - 1) / kXcds * kXcds : blocks;
+  dim3 grid(static_cast<uint32_t>(grid_x), slabs);
   hipLaunchKernelGGL((forward_kernel<WT, EPL, U, TAB, SIGN>), grid, dim3(kBlockThreads), 0, stream,
-                     w, p, indices, offsets, out);
+                     w, p, indices, offsets, out, xcd_split);
   return hipGetLastError();
 }
 

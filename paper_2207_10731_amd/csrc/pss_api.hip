@@ -264,13 +264,16 @@ int prepare_backward(const KParams& p, const void* indices, const void* offsets,
   }
   std::lock_guard<std::mutex> lock(pr->mu);
   pr->valid = false;
-  // created on first use (each one again if an earlier creation failed)
+  // created on first use (each one again if an earlier creation failed);
+  // both events order work on this device only, so they release at device
+  // scope (a system-scope release would write back the L2s for the host)
   if (pr->side == nullptr && hipStreamCreateWithFlags(&pr->side, hipStreamNonBlocking) != hipSuccess) {
     pr->side = nullptr;
     return PSS_ERR_HIP;
   }
   for (hipEvent_t* ev : {&pr->start, &pr->ready}) {
-    if (*ev == nullptr && hipEventCreateWithFlags(ev, hipEventDisableTiming) != hipSuccess) {
+    if (*ev == nullptr &&
+        hipEventCreateWithFlags(ev, hipEventDisableTiming | hipEventReleaseToDevice) != hipSuccess) {
       *ev = nullptr;
       return PSS_ERR_HIP;
     }

@@ -21,7 +21,6 @@
 
 namespace pss {
 
-constexpr uint64_t kXcds = 8;  // XCDs of an MI355X
 // Shared arrays larger than the chip's aggregate L2 (8 x 4 MiB) get their
 // tiles partitioned over the XCDs (see forward_kernel).  Measured: the
 // multi-hot forward on a 64 MB array 1053 -> 867 us, the row-hash forward

@@ -22,6 +22,7 @@ constexpr int kWave = 64;
 constexpr int kTileBags = 64;     // bags per wavefront tile
 constexpr int kBlockThreads = 256;  // 4 wavefronts per workgroup
 constexpr int kWavesPerBlock = kBlockThreads / kWave;
+constexpr uint64_t kXcds = 8;  // XCDs of an MI355X, each with an L2 of its own
 
 struct KParams {
   uint64_t fm_c;      // fast-mod constant of M

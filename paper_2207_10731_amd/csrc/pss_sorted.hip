@@ -33,6 +33,18 @@ constexpr int kWaveSortKeys = kWave * kSortItemsPerLane;       // keys per wave
 constexpr int kDigitsPerThread = kBins / kBlockThreads;
 static_assert(kBins % kBlockThreads == 0, "whole digits per thread in the scatter prologue");
 
+// Sort tile of this workgroup.  Workgroups are dispatched to the XCDs in
+// turn (workgroup i to XCD i mod kXcds), and each XCD has an L2 of its own.
+// Numbered this way, XCD x takes the contiguous tiles [x * per_xcd,
+// (x + 1) * per_xcd): the count words and digit runs of neighbouring tiles,
+// which lie side by side in memory, are then written through one L2 and
+// leave it as whole lines.  The grid holds kXcds * per_xcd workgroups;
+// those whose tile is at or past the last do nothing.  Any other dispatch
+// order only changes which L2 a tile's writes pass through.
+__device__ __forceinline__ uint32_t sort_tile_index(const uint32_t per_xcd) {
+  return (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+}
+
 // ---------------------------------------------------------------------------
 // keygen
 // ---------------------------------------------------------------------------
@@ -103,21 +115,24 @@ __device__ __forceinline__ int64_t live_count(int64_t n, const uint32_t* n_dev) 
   return d < n ? d : n;
 }
 
-// counts[d * nblocks + blk] = number of keys of tile blk with digit d.
+// counts[d * nblocks + tile] = number of keys of the tile with digit d.
 __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
     const uint32_t* __restrict__ keys, int64_t n, const int shift,
-    uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t* __restrict__ n_dev) {
+    uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t per_xcd,
+    const uint32_t* __restrict__ n_dev) {
+  const uint32_t tile = sort_tile_index(per_xcd);
+  if (tile >= nblocks) return;
   n = live_count(n, n_dev);
-  if (static_cast<int64_t>(blockIdx.x) * kSortTile >= n) {  // no live key in this tile
+  if (static_cast<int64_t>(tile) * kSortTile >= n) {  // no live key in this tile
     for (int d = threadIdx.x; d < kBins; d += kBlockThreads)
-      counts[static_cast<uint64_t>(d) * nblocks + blockIdx.x] = 0;
+      counts[static_cast<uint64_t>(d) * nblocks + tile] = 0;
     return;
   }
   __shared__ uint32_t hist[kWavesPerBlock][kBins];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
   __syncthreads();
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSortTile + w * kWaveSortKeys;
+  const int64_t base = static_cast<int64_t>(tile) * kSortTile + w * kWaveSortKeys;
 #pragma unroll 4
   for (int s = 0; s < kSortItemsPerLane; ++s) {
     const int64_t idx = base + s * kWave + lane;
@@ -132,7 +147,7 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
     uint32_t s = 0;
 #pragma unroll
     for (int ww = 0; ww < kWavesPerBlock; ++ww) s += hist[ww][d];
-    counts[static_cast<uint64_t>(d) * nblocks + blockIdx.x] = s;
+    counts[static_cast<uint64_t>(d) * nblocks + tile] = s;
   }
 }
 
@@ -145,8 +160,8 @@ __device__ __forceinline__ int64_t load_int(const void* a, uint64_t i) {
 
 // Keygen in item space for batches with as many items as bags, fused with
 // the first radix pass's histogram: workgroup blk takes the sort tile of
-// items [blk * kSortTile, ...), writes their (key, row) pairs and the tile's
-// digit counts of the low kSortBits bits (counts[d * nblocks + blk]).  When
+// items [tile * kSortTile, ...), writes their (key, row) pairs and the tile's
+// digit counts of the low kSortBits bits (counts[d * nblocks + tile]).  When
 // every item of the tile is its own bag (offsets[e] == e), item e belongs
 // to bag e; otherwise each item finds its bag by binary search over the
 // offsets (the largest g with offsets[g] <= e).
@@ -154,8 +169,10 @@ template <bool I32>
 __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
     uint32_t* __restrict__ keys, uint32_t* __restrict__ rows, float* __restrict__ inv_len,
-    uint32_t* __restrict__ counts, const uint32_t nblocks) {
-  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSortTile;
+    uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t per_xcd) {
+  const uint32_t tile = sort_tile_index(per_xcd);
+  if (tile >= nblocks) return;
+  const int64_t tile0 = static_cast<int64_t>(tile) * kSortTile;
   const int in_tile = p.N - tile0 < kSortTile ? static_cast<int>(p.N - tile0) : kSortTile;
   __shared__ uint32_t hist[kWavesPerBlock][kBins];
   __shared__ int irregular;
@@ -229,7 +246,7 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     uint32_t c = 0;
 #pragma unroll
     for (int ww = 0; ww < kWavesPerBlock; ++ww) c += hist[ww][d];
-    counts[static_cast<uint64_t>(d) * nblocks + blockIdx.x] = c;
+    counts[static_cast<uint64_t>(d) * nblocks + tile] = c;
   }
 }
 
@@ -274,10 +291,13 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
     const int shift, const uint32_t* __restrict__ offsets, const uint32_t nblocks,
-    const uint32_t* __restrict__ totals, const uint32_t* __restrict__ n_dev) {
+    const uint32_t* __restrict__ totals, const uint32_t per_xcd,
+    const uint32_t* __restrict__ n_dev) {
+  const uint32_t tile = sort_tile_index(per_xcd);
+  if (tile >= nblocks) return;
   n = live_count(n, n_dev);
   // tiles wholly past the live keys hold nothing (their counts are zero)
-  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kSortTile;
+  const int64_t tile0 = static_cast<int64_t>(tile) * kSortTile;
   if (tile0 >= n) return;
   const int in_tile = n - tile0 < kSortTile ? static_cast<int>(n - tile0) : kSortTile;
   __shared__ uint32_t cur[kWavesPerBlock][kBins];
@@ -292,7 +312,7 @@ __global__ __launch_bounds__(kBlockThreads) void sort_scatter_kernel(
   // with the tile's pairs (one wait for memory)
   const int d = threadIdx.x;
   const uint32_t total_d = totals[d];
-  const uint32_t offset_d = offsets[static_cast<uint64_t>(d) * nblocks + blockIdx.x];
+  const uint32_t offset_d = offsets[static_cast<uint64_t>(d) * nblocks + tile];
   uint32_t k[kSortItemsPerLane], v[kSortItemsPerLane];
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
@@ -653,6 +673,11 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
   }
 }
 
+// Sort tiles per XCD in the numbering of sort_tile_index.
+static uint32_t sort_tiles_per_xcd(uint32_t nblocks) {
+  return static_cast<uint32_t>((nblocks + kXcds - 1) / kXcds);
+}
+
 size_t radix_scratch_bytes(int64_t n) {
   const uint64_t nblocks = (static_cast<uint64_t>(n) + kSortTile - 1) / kSortTile;
   return (nblocks * kBins + kBins) * 4 + 256;
@@ -669,16 +694,18 @@ hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, ui
                             const uint32_t* n_dev, bool first_counted) {
   if (n == 0) return hipSuccess;
   const uint32_t nblocks = static_cast<uint32_t>((n + kSortTile - 1) / kSortTile);
+  const uint32_t per_xcd = sort_tiles_per_xcd(nblocks);
+  const dim3 grid(per_xcd * static_cast<uint32_t>(kXcds));
   uint32_t* counts = scratch;
   uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
   for (int shift = 0; shift < bits; shift += kSortBits) {
     if (shift > 0 || !first_counted)
-      hipLaunchKernelGGL(sort_hist_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys, n,
-                         shift, counts, nblocks, n_dev);
+      hipLaunchKernelGGL(sort_hist_kernel, grid, dim3(kBlockThreads), 0, stream, keys, n, shift,
+                         counts, nblocks, per_xcd, n_dev);
     hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
                        nblocks, totals);
-    hipLaunchKernelGGL(sort_scatter_kernel, dim3(nblocks), dim3(kBlockThreads), 0, stream, keys,
-                       vals, ktmp, vtmp, n, shift, counts, nblocks, totals, n_dev);
+    hipLaunchKernelGGL(sort_scatter_kernel, grid, dim3(kBlockThreads), 0, stream, keys, vals,
+                       ktmp, vtmp, n, shift, counts, nblocks, totals, per_xcd, n_dev);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     uint32_t* t = keys; keys = ktmp; ktmp = t;
@@ -761,12 +788,14 @@ hipError_t launch_group_sorted(const KParams& p, const void* indices, const void
   hipError_t e = hipSuccess;
   if (item_space) {
     const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
+    const uint32_t per_xcd = sort_tiles_per_xcd(nblocks);
+    const dim3 grid(per_xcd * static_cast<uint32_t>(kXcds));
     if (p.idx32)
-      hipLaunchKernelGGL(keygen_hist_kernel<true>, dim3(nblocks), dim3(kBlockThreads), 0, stream,
-                         p, indices, offsets, k0, v0, inv_len, scratch, nblocks);
+      hipLaunchKernelGGL(keygen_hist_kernel<true>, grid, dim3(kBlockThreads), 0, stream, p,
+                         indices, offsets, k0, v0, inv_len, scratch, nblocks, per_xcd);
     else
-      hipLaunchKernelGGL(keygen_hist_kernel<false>, dim3(nblocks), dim3(kBlockThreads), 0, stream,
-                         p, indices, offsets, k0, v0, inv_len, scratch, nblocks);
+      hipLaunchKernelGGL(keygen_hist_kernel<false>, grid, dim3(kBlockThreads), 0, stream, p,
+                         indices, offsets, k0, v0, inv_len, scratch, nblocks, per_xcd);
     e = hipGetLastError();
   } else {
     e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);

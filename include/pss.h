@@ -242,7 +242,6 @@ int pss_hash_signs_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
  * offsets[T*B] == N.  Returns PSS_OK or PSS_ERR_INVALID_ARG. */
 int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N);
 
-/* Static, NUL-terminated description of a status code. */
 /* Frees the scratch buffers kept between calls, and the streams, events and
  * buffers of PSS_PREPARE_BACKWARD (see "Memory" above), on every device that
  * holds them, after waiting for that device's work to finish.  Host only; no
@@ -251,6 +250,7 @@ int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t 
  * PSS_ERR_HIP if a runtime call fails (everything is forgotten either way). */
 int pss_release_scratch(void);
 
+/* Static, NUL-terminated description of a status code. */
 const char* pss_status_string(int status);
 
 #ifdef __cplusplus

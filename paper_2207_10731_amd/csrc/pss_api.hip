@@ -123,7 +123,10 @@ hipError_t pool_for_current_device(hipMemPool_t* out) {
   if (st != hipSuccess) return st;
   uint64_t threshold = UINT64_MAX;
   st = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
-  if (st != hipSuccess) return st;
+  if (st != hipSuccess) {
+    (void)hipMemPoolDestroy(pool);
+    return st;
+  }
   g_pools[dev] = pool;
   *out = pool;
   return hipSuccess;

@@ -126,6 +126,30 @@ def _need(t, dtype, name, device=True):
         raise ValueError(f"{name} must be a GPU tensor")
 
 
+def _need_len(t, n, name):
+    """The kernels trust the sizes the call declares (M, N, T*B, d): a tensor
+    shorter than that would be read or written past its end."""
+    if t is not None and t.numel() < n:
+        raise ValueError(f"{name} has {t.numel()} elements, the call needs {n}")
+
+
+def _same_device(*ts):
+    """Scratch, pools and launches follow the current device."""
+    dev = torch.cuda.current_device()
+    for t in ts:
+        if t is not None and t.is_cuda and t.device.index != dev:
+            raise ValueError(f"tensor on {t.device}, current device is cuda:{dev}")
+
+
+def _need_batch(hash_params, M, Z, d, indices, offsets, rows=None, rows_name="out"):
+    """Sizes the call implies: indices N, offsets T*B + 1, rows B x T*d."""
+    bags = int(hash_params.num_tables) * int(hash_params.batch)
+    _need_len(indices, int(hash_params.num_indices), "indices")
+    _need_len(offsets, bags + 1, "offsets")
+    if rows is not None:
+        _need_len(rows, bags * int(d), rows_name)
+
+
 def make_hash_params(seed=None, *, a=None, b=None, sign_a=None, sign_b=None, num_tables, batch,
                      num_indices, weight_dtype=PSS_F32, eps=1e-10,
                      flags=PSS_BWD_AUTO) -> pss_hash_params:
@@ -163,6 +187,9 @@ def pss_forward(shared, M, Z, d, hash_params, indices, offsets, out, stream=None
     _need(indices, _index_dtype(hash_params), "indices")
     _need(offsets, _index_dtype(hash_params), "offsets")
     _need(out, _row_dtype(hash_params), "out")
+    _need_len(shared, M, "shared")
+    _need_batch(hash_params, M, Z, d, indices, offsets, out, "out")
+    _same_device(shared, indices, offsets, out)
     _check(lib.pss_forward(_ptr(shared), M, Z, d, ctypes.byref(hash_params), _ptr(indices),
                            _ptr(offsets), _ptr(out), _stream(stream)), "pss_forward")
     return out
@@ -178,6 +205,10 @@ def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, g
     _need(indices, _index_dtype(hash_params), "indices")
     _need(offsets, _index_dtype(hash_params), "offsets")
     _need(grad_out, _row_dtype(hash_params), "grad_out")
+    _need_len(shared, M, "shared")
+    _need_len(state, M, "state")
+    _need_batch(hash_params, M, Z, d, indices, offsets, grad_out, "grad_out")
+    _same_device(shared, state, indices, offsets, grad_out)
     _check(lib.pss_backward_update(_ptr(shared), _ptr(state), M, Z, d, ctypes.byref(hash_params),
                                    _ptr(indices), _ptr(offsets), _ptr(grad_out),
                                    ctypes.c_float(lr), _stream(stream)), "pss_backward_update")
@@ -196,6 +227,9 @@ def pss_gradient_sparse(M, Z, d, hash_params, indices, offsets, grad_out, locati
     _need(num_unique, torch.int64, "num_unique")
     if locations.numel() != values.numel():
         raise ValueError("locations and values must have the same length")
+    _need_len(num_unique, 1, "num_unique")
+    _need_batch(hash_params, M, Z, d, indices, offsets, grad_out, "grad_out")
+    _same_device(indices, offsets, grad_out, locations, values, num_unique)
     _check(lib.pss_gradient_sparse(M, Z, d, ctypes.byref(hash_params), _ptr(indices), _ptr(offsets),
                                    _ptr(grad_out), _ptr(locations), _ptr(values),
                                    locations.numel(), _ptr(num_unique), _stream(stream)),
@@ -207,6 +241,10 @@ def pss_debug_addresses(M, Z, d, hash_params, indices, offsets, base_out, stream
     _need(indices, _index_dtype(hash_params), "indices")
     _need(offsets, _index_dtype(hash_params), "offsets")
     _need(base_out, torch.int32, "base_out")  # uint32 bit patterns
+    _need_batch(hash_params, M, Z, d, indices, offsets)
+    if Z > 0 and d % Z == 0:
+        _need_len(base_out, int(hash_params.num_indices) * (d // Z), "base_out")
+    _same_device(indices, offsets, base_out)
     _check(lib.pss_debug_addresses(M, Z, d, ctypes.byref(hash_params), _ptr(indices),
                                    _ptr(offsets), _ptr(base_out), _stream(stream)),
            "pss_debug_addresses")
@@ -218,6 +256,10 @@ def pss_debug_signs(M, Z, d, hash_params, indices, offsets, sign_out, stream=Non
     _need(indices, _index_dtype(hash_params), "indices")
     _need(offsets, _index_dtype(hash_params), "offsets")
     _need(sign_out, torch.int8, "sign_out")
+    _need_batch(hash_params, M, Z, d, indices, offsets)
+    if Z > 0 and d % Z == 0:
+        _need_len(sign_out, int(hash_params.num_indices) * (d // Z), "sign_out")
+    _same_device(indices, offsets, sign_out)
     _check(lib.pss_debug_signs(M, Z, d, ctypes.byref(hash_params), _ptr(indices), _ptr(offsets),
                                _ptr(sign_out), _stream(stream)), "pss_debug_signs")
     return sign_out
@@ -230,6 +272,10 @@ def pss_hash_bases_host(M, Z, d, hash_params, indices, offsets):
     idx = np.ascontiguousarray(indices, dtype=np.int64)
     off = np.ascontiguousarray(offsets, dtype=np.int64)
     out = np.zeros((idx.shape[0], d // Z if Z > 0 and d % Z == 0 else 1), dtype=np.uint32)
+    if idx.shape[0] < int(hash_params.num_indices):
+        raise ValueError(f"indices has {idx.shape[0]} entries, the call needs {hash_params.num_indices}")
+    if off.shape[0] < int(hash_params.num_tables) * int(hash_params.batch) + 1:
+        raise ValueError("offsets must hold T*B + 1 entries")
     _check(lib.pss_hash_bases_host(M, Z, d, ctypes.byref(hash_params),
                                    idx.ctypes.data_as(ctypes.c_void_p),
                                    off.ctypes.data_as(ctypes.c_void_p),
@@ -244,6 +290,10 @@ def pss_hash_signs_host(M, Z, d, hash_params, indices, offsets):
     idx = np.ascontiguousarray(indices, dtype=np.int64)
     off = np.ascontiguousarray(offsets, dtype=np.int64)
     out = np.zeros((idx.shape[0], d // Z if Z > 0 and d % Z == 0 else 1), dtype=np.int8)
+    if idx.shape[0] < int(hash_params.num_indices):
+        raise ValueError(f"indices has {idx.shape[0]} entries, the call needs {hash_params.num_indices}")
+    if off.shape[0] < int(hash_params.num_tables) * int(hash_params.batch) + 1:
+        raise ValueError("offsets must hold T*B + 1 entries")
     _check(lib.pss_hash_signs_host(M, Z, d, ctypes.byref(hash_params),
                                    idx.ctypes.data_as(ctypes.c_void_p),
                                    off.ctypes.data_as(ctypes.c_void_p),
@@ -254,6 +304,8 @@ def pss_hash_signs_host(M, Z, d, hash_params, indices, offsets):
 def pss_validate_offsets_host(offsets, num_bags, N) -> int:
     import numpy as np
     off = np.ascontiguousarray(offsets, dtype=np.int64)
+    if num_bags < 0 or off.shape[0] < num_bags + 1:
+        return PSS_ERR_INVALID_ARG
     return load_library().pss_validate_offsets_host(off.ctypes.data_as(ctypes.c_void_p),
                                                     num_bags, N)
 

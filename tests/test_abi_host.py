@@ -190,3 +190,19 @@ def test_offsets_validator():
     assert pss.pss_validate_offsets_host(np.array([0, 2, 1, 3]), 3, 3) == pss.PSS_ERR_INVALID_ARG
     assert pss.pss_validate_offsets_host(np.array([1, 2, 2, 3]), 3, 3) == pss.PSS_ERR_INVALID_ARG
     assert pss.pss_validate_offsets_host(np.array([0, 1, 2, 3]), 3, 4) == pss.PSS_ERR_INVALID_ARG
+    # shorter than num_bags + 1 entries: rejected before the library reads it
+    assert pss.pss_validate_offsets_host(np.array([0, 1, 3]), 3, 3) == pss.PSS_ERR_INVALID_ARG
+
+
+def test_host_hash_rejects_short_arrays():
+    """The host hash entry points read N indices and T*B + 1 offsets: the
+    binding refuses arrays shorter than the sizes the parameters declare."""
+    hp = pss.make_hash_params(7, num_tables=2, batch=3, num_indices=6)
+    idx = np.arange(6)
+    off = np.arange(7)
+    for fn in (pss.pss_hash_bases_host, pss.pss_hash_signs_host):
+        assert fn(64, 4, 8, hp, idx, off).shape == (6, 2)
+        with pytest.raises(ValueError):
+            fn(64, 4, 8, hp, idx[:5], off)
+        with pytest.raises(ValueError):
+            fn(64, 4, 8, hp, idx, off[:6])

@@ -1,0 +1,132 @@
+"""The largest shared array the ABI accepts: M = p = 2^31 - 1 float32
+elements (8.6 GB).  Indices are chosen so that chunks start at elements
+M - 1, M - Z + 1 (both wrap to element 0), M - Z (ends exactly at M - 1) and
+0, next to the extreme index values 0 and 2^31 - 1 and random ones, in bags
+of zero to four items.  The forward is checked against the oracle on every
+bag, and each backward variant (SGD and Adagrad) on every element the batch
+reads, the elements around the wrap, and random untouched ones."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import pss_oracle as o
+from paper_2207_10731_amd import pss
+
+pytestmark = pytest.mark.gpu
+
+P = 2**31 - 1
+M = P
+Z, D, T, B = 8, 32, 4, 256
+C = D // Z
+SEED = 2207
+LR, EPS = 0.05, 1e-10
+RTOL = 1e-5
+
+
+def _index_for_base(a, b, t, base):
+    """An index i of table t whose chunk 0 starts at `base`: the key of chunk
+    0 is i*T*C + t*C, and with M = p the base is (a*key + b) mod p."""
+    key = (base - b) * pow(a, P - 2, P) % P
+    return (key - t * C) * pow(T * C, P - 2, P) % P
+
+
+@pytest.fixture(scope="module")
+def batch():
+    a, b = o.hash_params_from_seed(SEED)
+    rng = np.random.default_rng(SEED)
+    lens = np.minimum(rng.poisson(1.5, T * B), 4)
+    lens[:8] = [1, 1, 2, 1, 0, 3, 1, 1]
+    offsets = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    N = int(offsets[-1])
+    t_of = np.repeat(np.arange(T * B) // B, lens)
+    idx = rng.integers(0, 2**31, N, dtype=np.int64)
+    # forced chunk starts (chunk 0 of the first items) and extreme indices
+    targets = [M - 1, M - Z + 1, M - Z, 0, M - 2]
+    for e, base in enumerate(targets):
+        idx[e] = _index_for_base(a, b, int(t_of[e]), base)
+    idx[len(targets)] = 0
+    idx[len(targets) + 1] = 2**31 - 1
+    base0 = o.bases_for(M, Z, D, T, a, b, idx[:len(targets)], t_of[:len(targets)])[:, 0]
+    assert list(base0) == targets  # checked on the host before any launch
+    return dict(a=a, b=b, idx=idx, off=offsets, N=N)
+
+
+def _setup(bt, flags):
+    dev = torch.device("cuda", 0)
+    gen = torch.Generator(device=dev).manual_seed(SEED)
+    shared = torch.randn(M, device=dev, generator=gen)
+    idx = torch.from_numpy(bt["idx"]).to(dev)
+    off = torch.from_numpy(bt["off"]).to(dev)
+    hp = pss.make_hash_params(a=bt["a"], b=bt["b"], num_tables=T, batch=B, num_indices=bt["N"],
+                              eps=EPS, flags=flags)
+    return dev, shared, idx, off, hp
+
+
+def _host_weights(shared, addr):
+    """Host array of M elements holding the device values at `addr` (the
+    others stay zero; the oracle reads no other element)."""
+    w = np.zeros(M, dtype=np.float32)  # pages are only touched where written
+    flat = np.unique(addr.reshape(-1))
+    w[flat] = shared[torch.from_numpy(flat).to(shared.device)].cpu().numpy()
+    return w
+
+
+def test_max_array_forward(batch):
+    dev, shared, idx, off, hp = _setup(batch, 0)
+    addr = o.element_addresses(M, Z, D, T, B, batch["a"], batch["b"], batch["idx"], batch["off"])
+    assert {M - 1, 0}.issubset(set(addr[:2].reshape(-1).tolist()))  # the wrap is read
+    out = torch.empty((B, T * D), device=dev)
+    print("max array: forward", flush=True)
+    pss.pss_forward(shared, M, Z, D, hp, idx, off, out)
+    torch.cuda.synchronize()
+    w = _host_weights(shared, addr)
+    ref, s_abs = o.forward64(w, M, Z, D, T, B, batch["a"], batch["b"], batch["idx"], batch["off"])
+    got = out.cpu().numpy().astype(np.float64)
+    bad = np.abs(got - ref) > RTOL * s_abs + 1e-30
+    assert not bad.any(), f"{bad.sum()} outputs out of tolerance"
+    del shared
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("opt", ["sgd", "adagrad"])
+@pytest.mark.parametrize("variant", [pss.PSS_BWD_ATOMIC, pss.PSS_BWD_SORTED, pss.PSS_BWD_SPARSE],
+                         ids=["atomic", "sorted", "sparse"])
+def test_max_array_backward(batch, variant, opt):
+    dev, shared, idx, off, hp = _setup(batch, variant)
+    state = torch.zeros(M, device=dev) if opt == "adagrad" else None
+    a, b = batch["a"], batch["b"]
+    addr = o.element_addresses(M, Z, D, T, B, a, b, batch["idx"], batch["off"])
+    rng = np.random.default_rng(SEED + 1)
+    where = np.unique(np.concatenate([addr.reshape(-1), rng.integers(0, M, 2000),
+                                      np.arange(M - Z - 2, M), np.arange(0, Z + 2)]))
+    wh = torch.from_numpy(where).to(dev)
+    w_old = shared[wh].cpu().numpy()
+    gen = torch.Generator(device=dev).manual_seed(SEED + 2)
+    g = torch.randn((B, T * D), device=dev, generator=gen)
+    grad = g.cpu().numpy()
+    print(f"max array: backward variant {variant} {opt}", flush=True)
+    pss.pss_backward_update(shared, state, M, Z, D, hp, idx, off, g, LR)
+    torch.cuda.synchronize()
+    w_gpu = shared[wh].cpu().numpy()
+    G, A, cnt = o.gradient_at(M, Z, D, T, B, a, b, batch["idx"], batch["off"], grad, where)
+    assert cnt[where == M - 1].item() > 0 and cnt[where == 0].item() > 0
+    w_old64 = w_old.astype(np.float64)
+    if state is None:
+        w_ref = o.sgd_update(w_old, G, LR)
+        bound = np.abs(w_old64) + LR * A
+        exempt = np.zeros(where.shape[0], dtype=bool)
+    else:
+        s_gpu = state[wh].cpu().numpy().astype(np.float64)
+        w_ref, s_ref = o.adagrad_update(w_old, np.zeros(where.shape[0], np.float32), G, LR, EPS)
+        assert np.all(np.abs(s_gpu - s_ref.astype(np.float64)) <= RTOL * A * A + 1e-30)
+        bound = np.abs(w_old64) + LR * A / (np.sqrt(s_ref.astype(np.float64)) + EPS)
+        exempt = np.abs(G) <= RTOL * A  # first step from s = 0: sign of a cancelled sum
+    err = np.abs(w_gpu.astype(np.float64) - w_ref.astype(np.float64))
+    bad = (err > RTOL * bound + 1e-30) & ~exempt
+    assert not bad.any(), f"{bad.sum()} of {where.shape[0]} weights out of tolerance"
+    untouched = cnt == 0
+    assert untouched.sum() > 1000
+    assert np.array_equal(w_gpu[untouched].view(np.uint32), w_old[untouched].view(np.uint32))
+    del shared, state, g
+    pss.pss_release_scratch()  # the G buffer of 8.6 GB is not kept for later tests
+    torch.cuda.empty_cache()

@@ -38,7 +38,8 @@ def test_addresses_bit_exact(case):
     assert np.array_equal(got.astype(np.uint64), want)
 
 
-@pytest.mark.parametrize("M", [4096, 2_500_000, 16_000_000, 64_000_000, 1_000_000_000])
+@pytest.mark.parametrize("M", [4096, 2_500_000, 16_000_000, 64_000_000, 1_000_000_000,
+                               2**31 - 2, 2**31 - 1])
 def test_fast_mod_exhaustive(M):
     """Every hash value h in [0, p) reduced mod M on the device equals torch's
     remainder (a = 1, b = 0, T = C = Z = 1 makes the base exactly h mod M)."""

@@ -2,11 +2,11 @@
 
 One step = pss_forward + pss_backward_update (forward gather/pool, backward
 deposit, optimizer step) over one batch of synthetic bags, rotating 4
-pre-generated index batches and gradient batches resident in HBM.  The
-forward carries PSS_PREPARE_BACKWARD (as a training loop would): the
-backward's grouping of the batch runs on a library stream beside the
-forward kernel and the backward reuses it (--no-prepare: the backward
-groups the batch itself).
+pre-generated index batches and gradient batches resident in HBM.  Each
+step starts with pss_prepare_backward (as a training loop would once the
+batch's indices are in place): the backward's grouping of the batch runs on
+a library stream beside the forward kernel and the backward reuses it
+(--no-prepare: the backward groups the batch itself).
 
 Default workload: criteo-tb-shaped one-hot batch (26 tables with log-uniform
 cardinalities in [3, 4e7], Zipf(1.1) indices, batch 65536, d = 128, Z = 32,
@@ -16,8 +16,10 @@ Prints one JSON line on stdout; diagnostics go to stderr.
   value          lookups/s over the timed steps (lookup = one (sample, table,
                  index) row: d gathered, pooled, d deposited)
   roofline       the dominant kernel's algorithmic HBM bytes per launch over
-                 its average duration (HIP events on the launch stream) vs the
-                 8 TB/s HBM peak; step_* fields give the same for the whole step.
+                 its average duration (HIP events on the launch stream, around
+                 the pss_forward call, which enqueues that one kernel there) vs
+                 the 8 TB/s HBM peak; step_* fields give the same for the whole
+                 step.
                  Events bracket the calls of every --event-every-th timed step
                  only: each event record costs the stream about 4 us, which
                  would otherwise be counted as step time.
@@ -151,7 +153,7 @@ def main():
     ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted", "sparse"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prepare", action="store_true",
-                    help="forward without PSS_PREPARE_BACKWARD")
+                    help="no pss_prepare_backward call: the backward groups the batch itself")
     ap.add_argument("--event-every", type=int, default=5,
                     help="time the calls of every n-th timed step with HIP events")
     args = ap.parse_args()
@@ -187,14 +189,15 @@ def main():
     gen.manual_seed(wl.data_seed)
     grads = [torch.randn((wl.B, wl.T * wl.d), generator=gen, device=dev) for _ in range(ROTATE)]
     out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=dev)
-    if not args.no_prepare:
-        flags |= pss.PSS_PREPARE_BACKWARD
+    prepare = not args.no_prepare
     hps = [pss.make_hash_params(wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=x.N,
                                 weight_dtype=dt_code, eps=wl.eps, flags=flags) for x in xs]
     torch.cuda.synchronize()
 
     def step(k, ev=None):
         r = k % ROTATE
+        if prepare:
+            pss.pss_prepare_backward(wl.M, wl.Z, wl.d, hps[r], idx[r], off[r])
         if ev is not None:
             ev[0].record()
         pss.pss_forward(shared, wl.M, wl.Z, wl.d, hps[r], idx[r], off[r], out)

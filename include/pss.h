@@ -44,8 +44,8 @@
  *   PSS_ROWS_BF16  out is written, and grad_out read, as bfloat16 (out is
  *     rounded to nearest even from the float32 result).
  *   PSS_PREPARE_BACKWARD  read by pss_forward only (the other calls ignore
- *     it): the forward also groups the batch's lookups by token for the
- *     backward, on a library-owned stream that runs beside the forward
+ *     it; pss_prepare_backward does the same work as a call of its own): the
+ *     forward also groups the batch's lookups by token for the backward, on a library-owned stream that runs beside the forward
  *     kernel.  The next pss_backward_update on the same stream uses that
  *     grouping when its indices and offsets pointers, batch shape, hash
  *     parameters and options match and it runs the SORTED variant (AUTO's
@@ -172,6 +172,25 @@ int pss_hash_params_from_seed(uint64_t seed, pss_hash_params* p);
 int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
                 const pss_hash_params* hash_params, const void* indices,
                 const void* offsets, void* out, hipStream_t stream);
+
+/* The grouping step of the backward's SORTED variant (paper Alg. 1: the
+ * lookups of a batch gathered by token before their gradients are summed),
+ * started ahead of the backward: what PSS_PREPARE_BACKWARD makes pss_forward
+ * do, as a call of its own, so that a caller can start it as soon as a
+ * batch's indices and offsets are ready (before the forward call, or
+ * without one).  It records an event on `stream` (everything enqueued there
+ * before this call completes before the grouping reads indices and
+ * offsets) and runs the grouping on a library-owned stream; the next
+ * pss_backward_update on `stream` uses it under the conditions given for
+ * PSS_PREPARE_BACKWARD, and the caller must not change the contents of
+ * indices or offsets until then.  Arguments as for pss_forward (the
+ * PSS_PREPARE_BACKWARD bit of hash_params->flags is not needed).  Does
+ * nothing and returns PSS_OK while `stream` is being captured into a graph,
+ * for N = 0 and for an explicit ATOMIC or SPARSE variant.  Returns
+ * PSS_ERR_NO_MEMORY or PSS_ERR_HIP if the grouping could not be set up (the
+ * backward then groups the batch itself). */
+int pss_prepare_backward(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                         const void* indices, const void* offsets, hipStream_t stream);
 
 /* Backward + optimizer step, in place (paper Sec. 2.4 backward, Alg. 1).
  *   G[m] = sum of s(e, j) * grad_out[b][t*d + j*Z + k] (divided by |bag| with

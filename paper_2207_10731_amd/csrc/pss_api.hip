@@ -383,6 +383,21 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
                                         offsets, out, stream));
 }
 
+int pss_prepare_backward(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
+                         const void* indices, const void* offsets, hipStream_t stream) {
+  const int st = check_common(M, Z, d, hash_params);
+  if (st != PSS_OK) return st;
+  if (offsets == nullptr) return PSS_ERR_INVALID_ARG;
+  if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
+  const KParams p = make_params(M, Z, d, hash_params);
+  const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
+  if (p.N == 0 || (variant != PSS_BWD_AUTO && variant != PSS_BWD_SORTED) || capturing(stream))
+    return PSS_OK;
+  const int ps = prepare_backward(p, indices, offsets, stream);
+  if (ps != PSS_OK) (void)hipGetLastError();
+  return ps;
+}
+
 int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
                         const pss_hash_params* hash_params, const void* indices,
                         const void* offsets, const void* grad_out, float lr,

@@ -65,6 +65,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_hash_params_from_seed.argtypes = [u64, hp]
     lib.pss_forward.argtypes = [vp, i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_backward_update.argtypes = [vp, vp, i64, i32, i32, hp, vp, vp, vp, ctypes.c_float, vp]
+    lib.pss_prepare_backward.argtypes = [i64, i32, i32, hp, vp, vp, vp]
     lib.pss_debug_addresses.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_debug_signs.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_hash_signs_host.argtypes = [i64, i32, i32, hp, vp, vp, vp]
@@ -75,7 +76,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_status_string.restype = ctypes.c_char_p
     lib.pss_release_scratch.argtypes = []
     for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
-                 "pss_debug_addresses", "pss_debug_signs", "pss_gradient_sparse",
+                 "pss_prepare_backward", "pss_debug_addresses", "pss_debug_signs",
+                 "pss_gradient_sparse",
                  "pss_hash_bases_host", "pss_hash_signs_host", "pss_validate_offsets_host",
                  "pss_release_scratch"):
         getattr(lib, name).restype = ctypes.c_int
@@ -193,6 +195,18 @@ def pss_forward(shared, M, Z, d, hash_params, indices, offsets, out, stream=None
     _check(lib.pss_forward(_ptr(shared), M, Z, d, ctypes.byref(hash_params), _ptr(indices),
                            _ptr(offsets), _ptr(out), _stream(stream)), "pss_forward")
     return out
+
+
+def pss_prepare_backward(M, Z, d, hash_params, indices, offsets, stream=None):
+    """Starts the backward's grouping of this batch on a library stream (the
+    work PSS_PREPARE_BACKWARD adds to pss_forward, as a call of its own)."""
+    lib = load_library()
+    _need(indices, _index_dtype(hash_params), "indices")
+    _need(offsets, _index_dtype(hash_params), "offsets")
+    _need_batch(hash_params, M, Z, d, indices, offsets)
+    _same_device(indices, offsets)
+    _check(lib.pss_prepare_backward(M, Z, d, ctypes.byref(hash_params), _ptr(indices),
+                                    _ptr(offsets), _stream(stream)), "pss_prepare_backward")
 
 
 def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr,

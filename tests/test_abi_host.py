@@ -206,3 +206,19 @@ def test_host_hash_rejects_short_arrays():
             fn(64, 4, 8, hp, idx[:5], off)
         with pytest.raises(ValueError):
             fn(64, 4, 8, hp, idx, off[:6])
+
+
+def test_prepare_rejects_bad_arguments(lib):
+    """pss_prepare_backward checks its arguments on the host before anything
+    is enqueued (the dummy pointers are never dereferenced)."""
+    dummy = ctypes.c_void_p(0x1000)
+
+    def call(M=4096, Z=4, d=16, a=5, T=4, B=2, N=8, offsets=dummy):
+        hp = pss.pss_hash_params(a, 7, T, B, N, 0, 1e-10, 0, 3, 11)
+        return lib.pss_prepare_backward(M, Z, d, ctypes.byref(hp), dummy, offsets, None)
+
+    assert call(M=0) == pss.PSS_ERR_INVALID_ARG
+    assert call(Z=5) == pss.PSS_ERR_INVALID_ARG  # Z does not divide d
+    assert call(a=0) == pss.PSS_ERR_INVALID_ARG
+    assert call(T=0) == pss.PSS_ERR_INVALID_ARG
+    assert call(offsets=None) == pss.PSS_ERR_INVALID_ARG

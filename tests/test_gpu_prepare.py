@@ -151,3 +151,34 @@ def test_backward_uses_the_grouping_made_by_the_forward():
         if grouped_batch == 1:
             L.x = other
         _check_update(L, g)
+
+
+@pytest.mark.parametrize("key,B,kw", [("c2", 700, {}), ("c3", 50, dict(mean=True))],
+                         ids=["onehot", "multihot-mean"])
+def test_explicit_prepare_call(key, B, kw):
+    """pss_prepare_backward, then a forward without the flag, then the
+    backward: the same results as without any preparation."""
+    L = Layer(synth.get(key), B=B, **kw)
+    wl = L.wl
+    g = synth.make_grad(wl, B=L.B)
+    pss.pss_prepare_backward(wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets)
+    _check_forward(L, L.forward())
+    L.backward(g)
+    _check_update(L, g)
+
+
+def test_explicit_prepare_is_used_by_the_backward():
+    """White box, as for the flag: after pss_prepare_backward (and a
+    synchronisation) the indices are overwritten in place with another
+    batch's, which the contract forbids; the backward still deposits at the
+    addresses of the batch that was grouped."""
+    L = Layer(synth.get("c2"), B=700, batch=0)
+    wl = L.wl
+    other = synth.make_inputs(wl, B=L.B, batch=1)
+    g = synth.make_grad(wl, B=L.B)
+    pss.pss_prepare_backward(wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets)
+    torch.cuda.synchronize()
+    L.indices.copy_(torch.from_numpy(other.indices).to(L.dev))
+    torch.cuda.synchronize()
+    L.backward(g)
+    _check_update(L, g)  # the oracle still sees batch 0

@@ -120,10 +120,6 @@ static hipError_t exclusive_scan(uint32_t* data, int64_t n, uint32_t* sums, uint
 // ---------------------------------------------------------------------------
 // runs of each 64-pair piece
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t lanes_upto(int lane) {  // lanes 0 .. lane
-  return lane == kWave - 1 ? ~0ull : ((1ull << (lane + 1)) - 1);
-}
-
 __global__ __launch_bounds__(kBlockThreads) void piece_runs_kernel(uint32_t* __restrict__ keys,
                                                                    uint32_t* __restrict__ rows,
                                                                    const int64_t n,

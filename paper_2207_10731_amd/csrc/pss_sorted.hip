@@ -40,9 +40,12 @@ static_assert(kBins % kBlockThreads == 0, "whole digits per thread in the scatte
 // which lie side by side in memory, are then written through one L2 and
 // leave it as whole lines.  The grid holds kXcds * per_xcd workgroups;
 // those whose tile is at or past the last do nothing.  Any other dispatch
-// order only changes which L2 a tile's writes pass through.
+// order only changes which L2 a tile's writes pass through.  per_xcd = 0
+// keeps tile = workgroup: a sort whose live keys are counted on the device
+// has its live tiles at the front, and contiguous ranges would put them all
+// on the first XCDs.
 __device__ __forceinline__ uint32_t sort_tile_index(const uint32_t per_xcd) {
-  return (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  return per_xcd ? (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds : blockIdx.x;
 }
 
 // ---------------------------------------------------------------------------
@@ -123,11 +126,8 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
   const uint32_t tile = sort_tile_index(per_xcd);
   if (tile >= nblocks) return;
   n = live_count(n, n_dev);
-  if (static_cast<int64_t>(tile) * kSortTile >= n) {  // no live key in this tile
-    for (int d = threadIdx.x; d < kBins; d += kBlockThreads)
-      counts[static_cast<uint64_t>(d) * nblocks + tile] = 0;
-    return;
-  }
+  // no live key in this tile: the scan reads the live tiles' counts only
+  if (static_cast<int64_t>(tile) * kSortTile >= n) return;
   __shared__ uint32_t hist[kWavesPerBlock][kBins];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
@@ -250,32 +250,39 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
   }
 }
 
-// Row d of counts (one digit, nblocks entries): exclusive scan in place;
-// totals[d] = the row's sum.  One workgroup per digit.
+// Row d of counts (one digit, one entry per tile): exclusive scan in place
+// over the tiles that hold live keys (the others are never read: their
+// scatter workgroups exit at once); totals[d] = the row's sum.  One
+// workgroup per digit.
 constexpr int kScanPerThread = 16;
 __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __restrict__ counts,
                                                                   const uint32_t nblocks,
-                                                                  uint32_t* __restrict__ totals) {
+                                                                  uint32_t* __restrict__ totals,
+                                                                  int64_t n,
+                                                                  const uint32_t* __restrict__ n_dev) {
   __shared__ uint32_t wsum[kWavesPerBlock];
+  n = live_count(n, n_dev);
+  const uint64_t live = (static_cast<uint64_t>(n) + kSortTile - 1) / kSortTile;
+  const uint32_t ntiles = live < nblocks ? static_cast<uint32_t>(live) : nblocks;
   uint32_t* row = counts + static_cast<uint64_t>(blockIdx.x) * nblocks;
   // entries per thread for this row (at most kScanPerThread per round)
-  const uint32_t per = (nblocks + kBlockThreads - 1) / kBlockThreads;
-  const uint32_t pt = per < kScanPerThread ? per : kScanPerThread;
+  const uint32_t per = (ntiles + kBlockThreads - 1) / kBlockThreads;
+  const uint32_t pt = per < 1 ? 1 : (per < kScanPerThread ? per : kScanPerThread);
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < nblocks; base += pt * kBlockThreads) {
+  for (uint32_t base = 0; base < ntiles; base += pt * kBlockThreads) {
     const uint32_t i0 = base + threadIdx.x * pt;
     uint32_t v[kScanPerThread];
     uint32_t sum = 0;
 #pragma unroll
     for (int j = 0; j < kScanPerThread; ++j) {
-      v[j] = (static_cast<uint32_t>(j) < pt && i0 + j < nblocks) ? row[i0 + j] : 0u;
+      v[j] = (static_cast<uint32_t>(j) < pt && i0 + j < ntiles) ? row[i0 + j] : 0u;
       sum += v[j];
     }
     uint32_t tot;
     uint32_t run = carry + block_exclusive_scan(sum, wsum, &tot);
 #pragma unroll
     for (int j = 0; j < kScanPerThread; ++j) {
-      if (static_cast<uint32_t>(j) < pt && i0 + j < nblocks) row[i0 + j] = run;
+      if (static_cast<uint32_t>(j) < pt && i0 + j < ntiles) row[i0 + j] = run;
       run += v[j];
     }
     carry += tot;
@@ -694,8 +701,10 @@ hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, ui
                             const uint32_t* n_dev, bool first_counted) {
   if (n == 0) return hipSuccess;
   const uint32_t nblocks = static_cast<uint32_t>((n + kSortTile - 1) / kSortTile);
-  const uint32_t per_xcd = sort_tiles_per_xcd(nblocks);
-  const dim3 grid(per_xcd * static_cast<uint32_t>(kXcds));
+  // live keys counted on the device fill a prefix of the tiles: numbered
+  // in dispatch order so that they spread over every XCD
+  const uint32_t per_xcd = n_dev == nullptr ? sort_tiles_per_xcd(nblocks) : 0u;
+  const dim3 grid(per_xcd ? per_xcd * static_cast<uint32_t>(kXcds) : nblocks);
   uint32_t* counts = scratch;
   uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
   for (int shift = 0; shift < bits; shift += kSortBits) {
@@ -703,7 +712,7 @@ hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, ui
       hipLaunchKernelGGL(sort_hist_kernel, grid, dim3(kBlockThreads), 0, stream, keys, n, shift,
                          counts, nblocks, per_xcd, n_dev);
     hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
-                       nblocks, totals);
+                       nblocks, totals, n, n_dev);
     hipLaunchKernelGGL(sort_scatter_kernel, grid, dim3(kBlockThreads), 0, stream, keys, vals,
                        ktmp, vtmp, n, shift, counts, nblocks, totals, per_xcd, n_dev);
     const hipError_t e = hipGetLastError();

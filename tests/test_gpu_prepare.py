@@ -93,8 +93,8 @@ def test_prepare_then_release():
 
 
 def test_prepared_step_in_a_graph():
-    """Forward with the flag and backward captured into one graph: under
-    capture the flag is ignored; three replays from the same weights, with
+    """Forward with the flag (and the explicit prepare call) and backward
+    captured into one graph: under capture both are ignored; three replays from the same weights, with
     eager prepared steps in between, each match the oracle."""
     dev = torch.device("cuda", 0)
     L = Layer(synth.get("c2"), B=300, flags=PREP)
@@ -112,6 +112,8 @@ def test_prepared_step_in_a_graph():
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
         s = torch.cuda.current_stream()
+        # the explicit call does nothing while the stream is being captured
+        pss.pss_prepare_backward(wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, stream=s)
         pss.pss_forward(L.shared, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, out, stream=s)
         pss.pss_backward_update(L.shared, None, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets,
                                 g_dev, wl.lr, stream=s)

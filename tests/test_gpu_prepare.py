@@ -184,3 +184,27 @@ def test_explicit_prepare_is_used_by_the_backward():
     torch.cuda.synchronize()
     L.backward(g)
     _check_update(L, g)  # the oracle still sees batch 0
+
+
+def test_prepared_on_two_streams():
+    """Groupings prepared on two streams at once for two batches: each
+    stream's backward reuses its own, and both match the oracle."""
+    dev = torch.device("cuda", 0)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    Ls = [Layer(synth.get("c2"), B=700, batch=k) for k in range(2)]
+    gs = [synth.make_grad(L.wl, B=L.B, batch=k) for k, L in enumerate(Ls)]
+    gd = [torch.from_numpy(g).to(dev) for g in gs]
+    outs = [torch.empty((L.B, L.wl.T * L.wl.d), device=dev) for L in Ls]
+    torch.cuda.synchronize()
+    for L, s in zip(Ls, streams):
+        wl = L.wl
+        pss.pss_prepare_backward(wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, stream=s)
+    for L, s, out, g in zip(Ls, streams, outs, gd):
+        wl = L.wl
+        pss.pss_forward(L.shared, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, out, stream=s)
+        pss.pss_backward_update(L.shared, None, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, g,
+                                wl.lr, stream=s)
+    torch.cuda.synchronize()
+    for L, out, g in zip(Ls, outs, gs):
+        _check_forward(L, out.cpu().numpy())
+        _check_update(L, g)

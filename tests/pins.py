@@ -18,6 +18,7 @@ Every ``pin_*`` function raises AssertionError when the oracle module ``o``
   pin_sparse_dense       Alg. 1 sparse branch, densified, equals dense branch
   pin_untouched          elements no lookup reads stay bit-identical
   pin_bf16_rounding      nearest-even bfloat16 rounding == torch's
+  pin_bf16_widening      bfloat16 -> float of every bit pattern == torch's
   pin_sign_and_mean      sign variants and mean pooling against the signed
                          sketch; torch's mean embedding_bag; SplitMix64
                          outputs 2-4; factor frequencies
@@ -295,6 +296,22 @@ def pin_bf16_rounding(o, seed=9):
     assert (int(nan[0]) & 0x7F80) == 0x7F80 and (int(nan[0]) & 0x7F) != 0
 
 
+def pin_bf16_widening(o):
+    """bfloat16 storage widened to a float (the weights every bf16 forward and
+    update reads): all 65,536 bit patterns (+-0, subnormals, +-inf, NaN
+    payloads, max-finite) against torch's own bfloat16 -> float32 conversion,
+    bit for bit."""
+    import torch
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = np.asarray(o.widen(bits, o.BF16), dtype=np.float64)
+    ref32 = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).float().numpy()
+    want = ref32.astype(np.float64)
+    assert np.array_equal(got.view(np.uint64), want.view(np.uint64))
+    # the sign bit alone distinguishes +-0 and the two halves of the table
+    assert np.signbit(got[0x8000]) and not np.signbit(got[0]) and got[0x8000] == 0.0
+    assert got[0x7F7F] == np.float64(np.float32(3.3895314e38)) and np.isinf(got[0x7F80])
+
+
 def pin_compress(o, seed=10):
     """M = S E and (S e_i)^T M against the explicit S; the injective case;
     eps of Def. 2 as the supremum it is defined to be; Thm. 1."""
@@ -436,4 +453,5 @@ def pin_sign_and_mean(o, seed=11):
 
 ALL_PINS = [pin_hash_vectors, pin_forward_brute, pin_gradient_brute, pin_integer_forward,
             pin_embedding_bag, pin_mass, pin_finite_difference, pin_sparse_dense,
-            pin_untouched, pin_bf16_rounding, pin_compress, pin_sign_and_mean]
+            pin_untouched, pin_bf16_rounding, pin_bf16_widening, pin_compress,
+            pin_sign_and_mean]

@@ -77,6 +77,23 @@ def _bf16_truncate(x):
     return (x32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
 
 
+_orig_widen = o.widen
+
+
+def _widen_bf16_drops_sign(w, weight_dtype=o.F32):
+    if weight_dtype != o.BF16:
+        return _orig_widen(w, weight_dtype)
+    bits = (np.asarray(w, dtype=np.uint16).astype(np.uint32) & np.uint32(0x7FFF)) << np.uint32(16)
+    return bits.view(np.float32).astype(np.float64)                     # sign bit dropped
+
+
+def _widen_bf16_shift15(w, weight_dtype=o.F32):
+    if weight_dtype != o.BF16:
+        return _orig_widen(w, weight_dtype)
+    bits = np.asarray(w, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+    return bits.view(np.float32).astype(np.float64)                     # off by one bit
+
+
 _orig_contrib = o._contributions
 
 
@@ -155,6 +172,8 @@ MUTANTS = {
     "sparse_signs_at_one_third": ("signs_for", _signs_threshold_third),
     "one_sign_per_item": ("signs_for", _signs_per_item),
     "gradient_ignores_mean": ("item_scale", _item_scale_ignores_mean),
+    "bf16_widen_drops_sign": ("widen", _widen_bf16_drops_sign),
+    "bf16_widen_shift_15": ("widen", _widen_bf16_shift15),
 }
 
 

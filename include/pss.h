@@ -45,13 +45,24 @@
  *     rounded to nearest even from the float32 result).
  *   PSS_PREPARE_BACKWARD  read by pss_forward only (the other calls ignore
  *     it; pss_prepare_backward does the same work as a call of its own): the
- *     forward also groups the batch's lookups by token for the backward, on a library-owned stream that runs beside the forward
- *     kernel.  The next pss_backward_update on the same stream uses that
- *     grouping when its indices and offsets pointers, batch shape, hash
- *     parameters and options match and it runs the SORTED variant (AUTO's
- *     choice for SGD on float32 storage); it drops the grouping either way.
- *     The caller must not change the contents of indices or offsets between
- *     the two calls.  Ignored while the stream is being captured into a
+ *     forward also groups the batch's lookups by token for the backward, on
+ *     a library-owned stream that runs beside the forward kernel.  The next
+ *     pss_backward_update on the same stream uses that grouping when its
+ *     indices and offsets pointers, batch shape, hash parameters and options
+ *     match and it runs the SORTED variant (AUTO's choice for SGD on float32
+ *     storage); it drops the grouping either way.  The match is by pointer:
+ *     the library records the indices and offsets pointers of the prepared
+ *     batch (comparing them later, never reading through them after the
+ *     grouping's own work) and cannot see their contents, so the caller must
+ *     not change the contents of indices or offsets between the two calls (a
+ *     backward on other contents at the same addresses would deposit at the
+ *     prepared batch's addresses).  A forward without the flag leaves a
+ *     prepared grouping in place, so that pss_prepare_backward, pss_forward
+ *     and pss_backward_update may follow each other.  When a grouping is
+ *     dropped unused (by a backward that does not match or cannot use it, or
+ *     by a new preparation on the same stream), `stream` first waits for it:
+ *     work the caller enqueues there afterwards follows its reads of the old
+ *     indices and offsets.  Ignored while the stream is being captured into a
  *     graph, and for an explicit ATOMIC or SPARSE variant; if the grouping
  *     cannot be set up (no memory for its buffer), the forward runs without
  *     it.  Holds one buffer of 16 B per lookup per stream (see "Memory").
@@ -61,7 +72,9 @@
  *   load and rounded to nearest-even once per update.
  * Memory.  Every array argument is device memory owned by the caller; the
  *   library keeps no pointer after the call returns other than in the work it
- *   enqueued.  Scratch space of the backward and sparse-gradient calls is a
+ *   enqueued, and the indices and offsets pointers that identify a prepared
+ *   grouping (compared by the next backward, never dereferenced by it).
+ *   Scratch space of the backward and sparse-gradient calls is a
  *   library-owned device buffer kept per (device, stream) between calls and
  *   grown to the largest call made on that stream (taken from a
  *   library-owned memory pool), and so does a forward call with
@@ -144,8 +157,9 @@ typedef struct {
   int64_t num_indices;   /* N = number of entries of `indices` (= offsets[T*B]) */
   int32_t weight_dtype;  /* pss_dtype of `shared` */
   float eps;             /* Adagrad epsilon (ignored by SGD); >= 0 */
-  uint32_t flags;        /* PSS_BWD_* in bits 0-1, options in bits 2-6; the
-                            sign field 3 << 2 and higher bits are invalid */
+  uint32_t flags;        /* PSS_BWD_* in bits 0-1, options in bits 2-7; the
+                            sign field value 3 << 2 and bits 8 and up are
+                            invalid */
   uint32_t sign_a;       /* sign hash multiplier, 1 <= sign_a <= p - 1
                             (read only when a sign option is set) */
   uint32_t sign_b;       /* sign hash offset, 0 <= sign_b <= p - 1 */
@@ -168,7 +182,7 @@ int pss_hash_params_from_seed(uint64_t seed, pss_hash_params* p);
  *          PSS_INDEX_I32)
  * out      device float32[B][T*d] (bfloat16 with PSS_ROWS_BF16), fully
  *          overwritten; must not alias inputs
- * T*(d/Z) must not exceed 2^32. */
+ * T*(d/Z) must be below 2^32. */
 int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
                 const pss_hash_params* hash_params, const void* indices,
                 const void* offsets, void* out, hipStream_t stream);
@@ -261,12 +275,16 @@ int pss_hash_signs_host(int64_t M, int32_t Z, int32_t d, const pss_hash_params* 
  * offsets[T*B] == N.  Returns PSS_OK or PSS_ERR_INVALID_ARG. */
 int pss_validate_offsets_host(const int64_t* offsets, int64_t num_bags, int64_t N);
 
-/* Frees the scratch buffers kept between calls, and the streams, events and
- * buffers of PSS_PREPARE_BACKWARD (see "Memory" above), on every device that
- * holds them, after waiting for that device's work to finish.  Host only; no
- * call of this library may be in progress on another thread.  Later calls
- * allocate afresh; a prepared grouping not yet used is dropped.  Returns
- * PSS_ERR_HIP if a runtime call fails (everything is forgotten either way). */
+/* Frees the scratch buffers kept between calls, the streams, events and
+ * buffers of PSS_PREPARE_BACKWARD and the library's memory pools (see
+ * "Memory" above), on every device that holds them, after waiting for that
+ * device's work to finish.  Host only; no call of this library may be in
+ * progress on another thread.  Later calls allocate afresh; a prepared
+ * grouping not yet used is dropped.  A program should call it before the
+ * HIP runtime shuts down (the Python binding does so at interpreter exit),
+ * so that the runtime's own teardown finds no library-owned object left.
+ * Returns PSS_ERR_HIP if a runtime call fails (everything is forgotten
+ * either way). */
 int pss_release_scratch(void);
 
 /* Static, NUL-terminated description of a status code. */

@@ -266,6 +266,13 @@ int prepare_backward(const KParams& p, const void* indices, const void* offsets,
     pr = &g_prep[{dev, reinterpret_cast<uintptr_t>(stream)}];
   }
   std::lock_guard<std::mutex> lock(pr->mu);
+  // A grouping that no backward used is dropped; the caller's stream first
+  // waits for it, so that work the caller orders after this call (freeing or
+  // refilling the old batch's indices) also follows the old grouping's reads.
+  if (pr->valid && hipStreamWaitEvent(stream, pr->ready, 0) != hipSuccess) {
+    pr->valid = false;
+    return PSS_ERR_HIP;
+  }
   pr->valid = false;
   // created on first use (each one again if an earlier creation failed);
   // both events order work on this device only, so they release at device
@@ -328,6 +335,11 @@ Prepared* take_prepared(hipStream_t stream, const void* indices, const void* off
   std::unique_lock<std::mutex> slot(pr->mu);
   const bool match = pr->valid && pr->indices == indices && pr->offsets == offsets &&
                      same_grouping(pr->made, p);
+  if (pr->valid && (!match || !usable)) {
+    // dropped unused: the caller's stream waits for the grouping (it may
+    // still be reading its batch's indices and offsets)
+    if (hipStreamWaitEvent(stream, pr->ready, 0) != hipSuccess) (void)hipGetLastError();
+  }
   pr->valid = false;
   if (!match || !usable) return nullptr;
   *lock = std::move(slot);
@@ -335,6 +347,83 @@ Prepared* take_prepared(hipStream_t stream, const void* indices, const void* off
 }
 
 int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; }
+
+// One backward call: the variant that runs and the scratch it needs.
+struct BackwardPlan {
+  KParams p;
+  uint32_t variant = PSS_BWD_SORTED;  // ATOMIC, SORTED or SPARSE
+  bool bf16 = false;
+  bool fused = false;   // SGD on float32 storage: deposits go into `shared`
+  size_t g_bytes = 0;   // float32 gradient buffer (unfused updates), 256-aligned
+  size_t ws_bytes = 0;  // grouping (SORTED) or sparse workspace, after it
+};
+constexpr int kNothingToDo = -1;  // no lookups: G == 0, nothing changes
+
+// Argument checks of the backward entry points (host only, before anything
+// is enqueued) and the plan.  Returns PSS_OK, kNothingToDo or an error.
+int plan_backward(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
+                  const pss_hash_params* hp, const void* indices, const void* offsets,
+                  const void* grad_out, float lr, BackwardPlan* plan) {
+  const int st = check_common(M, Z, d, hp);
+  if (st != PSS_OK) return st;
+  if (shared == nullptr || offsets == nullptr || grad_out == nullptr) return PSS_ERR_INVALID_ARG;
+  if (indices == nullptr && hp->num_indices > 0) return PSS_ERR_INVALID_ARG;
+  if (!isfinite(lr)) return PSS_ERR_INVALID_ARG;
+  if (state != nullptr && !(hp->eps >= 0.f && isfinite(hp->eps))) return PSS_ERR_INVALID_ARG;
+  plan->p = make_params(M, Z, d, hp);
+  const KParams& p = plan->p;
+  plan->bf16 = hp->weight_dtype == PSS_BF16;
+  const bool sparse_fits = p.N * static_cast<int64_t>(p.C) < (1ll << 31);
+  uint32_t variant = hp->flags & PSS_BWD_MASK;
+  if (variant == PSS_BWD_SPARSE && !sparse_fits) return PSS_ERR_UNSUPPORTED;
+  if (p.N == 0) return kNothingToDo;
+  if (variant == PSS_BWD_AUTO) variant = auto_variant(M, p, state != nullptr || plan->bf16, sparse_fits);
+  plan->variant = variant;
+  if (variant == PSS_BWD_SPARSE) {
+    // Alg. 1 sparse branch: 256 bytes for the unique count, then its workspace
+    plan->ws_bytes = 256 + pss::sparse_workspace_bytes(p);
+    return PSS_OK;
+  }
+  // SGD on float32 storage is linear in G: deposit -lr * grad directly into
+  // the shared array.  Otherwise deposit G into a scratch buffer first.
+  plan->fused = state == nullptr && !plan->bf16;
+  plan->g_bytes = plan->fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
+  plan->ws_bytes = variant == PSS_BWD_SORTED ? pss::sorted_workspace_bytes(p) : 0;
+  return PSS_OK;
+}
+
+// Enqueues the planned backward on `stream`.  ws: scratch of at least
+// plan.g_bytes + plan.ws_bytes bytes; prep: a grouping made ahead for this
+// batch (SORTED only), or null.
+hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state, float eps,
+                            const void* indices, const void* offsets, const void* grad_out,
+                            float lr, void* ws, Prepared* prep, hipStream_t stream) {
+  const KParams& p = plan.p;
+  if (plan.variant == PSS_BWD_SPARSE) {
+    // the optimizer is applied at each unique location as it is summed
+    uint32_t* count = static_cast<uint32_t*>(ws);
+    return pss::launch_sparse_update(p, indices, offsets, grad_out, static_cast<char*>(ws) + 256,
+                                     count, shared, plan.bf16, state, lr, eps, stream);
+  }
+  float* dst = plan.fused ? static_cast<float*>(shared) : static_cast<float*>(ws);
+  void* sort_ws = static_cast<char*>(ws) + plan.g_bytes;
+  const float scale = plan.fused ? -lr : 1.f;
+  const int64_t M = p.M;
+  hipError_t e = hipSuccess;
+  if (!plan.fused) e = pss::launch_zero(dst, M, stream);
+  if (e == hipSuccess && prep != nullptr) {
+    // the grouping ran on the library stream during the forward
+    e = hipStreamWaitEvent(stream, prep->ready, 0);
+    if (e == hipSuccess) e = pss::launch_reduce_sorted(dst, scale, p, prep->pairs, grad_out, stream);
+  } else if (e == hipSuccess) {
+    e = plan.variant == PSS_BWD_SORTED
+            ? pss::launch_deposit_sorted(dst, scale, p, indices, offsets, grad_out, sort_ws, stream)
+            : pss::launch_deposit_atomic(dst, scale, p, indices, offsets, grad_out, stream);
+  }
+  if (e == hipSuccess && !plan.fused)
+    e = pss::launch_optimizer(shared, plan.bf16, state, dst, M, lr, eps, stream);
+  return e;
+}
 
 uint64_t splitmix64_next(uint64_t* state) {
   uint64_t z = (*state += 0x9E3779B97F4A7C15ull);
@@ -402,71 +491,23 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
                         const pss_hash_params* hash_params, const void* indices,
                         const void* offsets, const void* grad_out, float lr,
                         hipStream_t stream) {
-  int st = check_common(M, Z, d, hash_params);
-  if (st != PSS_OK) return st;
-  if (shared == nullptr || offsets == nullptr || grad_out == nullptr) return PSS_ERR_INVALID_ARG;
-  if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
-  if (!isfinite(lr)) return PSS_ERR_INVALID_ARG;
-  if (state != nullptr && !(hash_params->eps >= 0.f && isfinite(hash_params->eps)))
-    return PSS_ERR_INVALID_ARG;
-  uint32_t variant = hash_params->flags & PSS_BWD_MASK;
-  const KParams p = make_params(M, Z, d, hash_params);
-  const bool bf16 = hash_params->weight_dtype == PSS_BF16;
-  const bool sparse_fits = p.N * static_cast<int64_t>(p.C) < (1ll << 31);
-  if (variant == PSS_BWD_SPARSE && !sparse_fits) return PSS_ERR_UNSUPPORTED;
-  if (p.N == 0) return PSS_OK;  // no lookups: G == 0, nothing changes
-  if (variant == PSS_BWD_AUTO) variant = auto_variant(M, p, state != nullptr || bf16, sparse_fits);
+  BackwardPlan plan;
+  const int st = plan_backward(shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr,
+                               &plan);
+  if (st != PSS_OK) return st == kNothingToDo ? PSS_OK : st;
   std::unique_lock<std::mutex> prep_lock;
-  Prepared* prep = take_prepared(stream, indices, offsets, p,
-                                 variant == PSS_BWD_SORTED && !capturing(stream), &prep_lock);
-
-  if (variant == PSS_BWD_SPARSE) {
-    // Alg. 1 sparse branch: unique locations + summed values, with the
-    // optimizer applied at each location as it is summed.
-    const size_t ws_bytes = pss::sparse_workspace_bytes(p);
-    CallScratch scratch;
-    st = scratch.take(256 + ws_bytes, stream);
-    if (st != PSS_OK) return st;
-    void* ws = scratch.ptr();
-    uint32_t* count = static_cast<uint32_t*>(ws);
-    hipError_t e = pss::launch_sparse_update(p, indices, offsets, grad_out,
-                                             static_cast<char*>(ws) + 256, count, shared, bf16,
-                                             state, lr, hash_params->eps, stream);
-    const hipError_t ef = scratch.done();
-    return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
-  }
-
-  const bool sorted = variant != PSS_BWD_ATOMIC;  // AUTO and SORTED
-
-  // SGD on float32 storage is linear in G: deposit -lr * grad directly into
-  // the shared array.  Otherwise deposit G into a scratch buffer first.
-  const bool fused = state == nullptr && !bf16;
-  const size_t g_bytes = fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
-  const size_t ws_bytes = (sorted && prep == nullptr) ? pss::sorted_workspace_bytes(p) : 0;
+  Prepared* prep = take_prepared(stream, indices, offsets, plan.p,
+                                 plan.variant == PSS_BWD_SORTED && !capturing(stream), &prep_lock);
+  if (prep != nullptr) plan.ws_bytes = 0;  // the grouping is already made
   CallScratch scratch;
-  if (g_bytes + ws_bytes > 0) {
-    st = scratch.take(g_bytes + ws_bytes, stream);
-    if (st != PSS_OK) return st;
+  if (plan.g_bytes + plan.ws_bytes > 0) {
+    const int ts = scratch.take(plan.g_bytes + plan.ws_bytes, stream);
+    if (ts != PSS_OK) return ts;
   }
-  void* ws = scratch.ptr();
-  float* dst = fused ? static_cast<float*>(shared) : static_cast<float*>(ws);
-  void* sort_ws = static_cast<char*>(ws) + g_bytes;
-  const float scale = fused ? -lr : 1.f;
-  hipError_t e = hipSuccess;
-  if (!fused) e = pss::launch_zero(dst, M, stream);
-  if (e == hipSuccess && prep != nullptr) {
-    // the grouping ran on the library stream during the forward
-    e = hipStreamWaitEvent(stream, prep->ready, 0);
-    if (e == hipSuccess) e = pss::launch_reduce_sorted(dst, scale, p, prep->pairs, grad_out, stream);
-  } else if (e == hipSuccess) {
-    e = sorted ? pss::launch_deposit_sorted(dst, scale, p, indices, offsets, grad_out, sort_ws, stream)
-               : pss::launch_deposit_atomic(dst, scale, p, indices, offsets, grad_out, stream);
-  }
-  if (e == hipSuccess && !fused)
-    e = pss::launch_optimizer(shared, bf16, state, dst, M, lr, hash_params->eps, stream);
+  const hipError_t e = enqueue_backward(plan, shared, state, hash_params->eps, indices, offsets,
+                                        grad_out, lr, scratch.ptr(), prep, stream);
   const hipError_t ef = scratch.done();
-  if (e != hipSuccess || ef != hipSuccess) return PSS_ERR_HIP;
-  return PSS_OK;
+  return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
 }
 
 int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
@@ -552,6 +593,16 @@ int pss_release_scratch(void) {
       if (pr.side != nullptr && hipStreamDestroy(pr.side) != hipSuccess) status = PSS_ERR_HIP;
     }
     g_prep.clear();
+  }
+  {
+    // the pools last: every buffer taken from them has been returned above
+    std::lock_guard<std::mutex> pool_lock(g_pool_mu);
+    for (auto& kv : g_pools) {
+      if (hipSetDevice(kv.first) != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
+          hipMemPoolDestroy(kv.second) != hipSuccess)
+        status = PSS_ERR_HIP;
+    }
+    g_pools.clear();
   }
   if (hipSetDevice(cur) != hipSuccess) status = PSS_ERR_HIP;
   return status;

@@ -7,6 +7,7 @@ be loaded, the first call raises.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
 import re
@@ -82,6 +83,41 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                  "pss_release_scratch"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
+    # Return the library's runtime objects (kept scratch, prepared-grouping
+    # streams and events, memory pools) while the interpreter still runs,
+    # before the HIP runtime's own teardown at process exit.
+    atexit.register(_release_at_exit)
+    return lib
+
+
+def _release_at_exit():
+    if _lib is not None:
+        try:
+            _lib.pss_release_scratch()
+        except Exception:  # nothing useful to do at exit
+            pass
+
+
+BENCH_LIB_PATH = os.path.join(_PKG, "libpss_bench.so")
+_bench = None
+
+
+def load_bench_library(path: str = BENCH_LIB_PATH) -> ctypes.CDLL:
+    """Loads libpss_bench.so (measurement kernels beside the layer) once."""
+    global _bench
+    if _bench is not None:
+        return _bench
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with python -m paper_2207_10731_amd.build")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.pss_bench_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]
+    lib.pss_bench_read.argtypes = [vp, ctypes.c_size_t, i32, i32, vp, vp]
+    lib.pss_bench_gather.argtypes = [vp, ctypes.c_size_t, i32, i32, ctypes.c_uint32, vp,
+                                     ctypes.POINTER(i64), vp]
+    for name in ("pss_bench_copy", "pss_bench_read", "pss_bench_gather"):
+        getattr(lib, name).restype = ctypes.c_int
+    _bench = lib
     return lib
 
 
@@ -211,6 +247,11 @@ def pss_prepare_backward(M, Z, d, hash_params, indices, offsets, stream=None):
 
 def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr,
                         stream=None):
+    _backward("pss_backward_update", shared, state, M, Z, d, hash_params, indices, offsets,
+              grad_out, lr, stream)
+
+
+def _backward(name, shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr, stream):
     lib = load_library()
     _need(shared, shared.dtype, "shared")
     if hash_params.weight_dtype != _weight_dtype(shared):
@@ -223,9 +264,9 @@ def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, g
     _need_len(state, M, "state")
     _need_batch(hash_params, M, Z, d, indices, offsets, grad_out, "grad_out")
     _same_device(shared, state, indices, offsets, grad_out)
-    _check(lib.pss_backward_update(_ptr(shared), _ptr(state), M, Z, d, ctypes.byref(hash_params),
-                                   _ptr(indices), _ptr(offsets), _ptr(grad_out),
-                                   ctypes.c_float(lr), _stream(stream)), "pss_backward_update")
+    _check(getattr(lib, name)(_ptr(shared), _ptr(state), M, Z, d, ctypes.byref(hash_params),
+                              _ptr(indices), _ptr(offsets), _ptr(grad_out), ctypes.c_float(lr),
+                              _stream(stream)), name)
 
 
 def pss_gradient_sparse(M, Z, d, hash_params, indices, offsets, grad_out, locations, values,

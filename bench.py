@@ -15,11 +15,18 @@ shared float32 array of 2.5e6 weights = 10 MB, SGD).
 Prints one JSON line on stdout; diagnostics go to stderr.
   value          lookups/s over the timed steps (lookup = one (sample, table,
                  index) row: d gathered, pooled, d deposited)
-  roofline       the dominant kernel's algorithmic HBM bytes per launch over
-                 its average duration (HIP events on the launch stream, around
-                 the pss_forward call, which enqueues that one kernel there) vs
-                 the 8 TB/s HBM peak; step_* fields give the same for the whole
-                 step.
+  roofline       the dominant kernel's floor bytes per launch over its
+                 average duration (HIP events on the launch stream, around the
+                 pss_forward call, which enqueues that one kernel there) vs the
+                 peak of the memory level that bounds it; step_* fields give
+                 the same for the whole step.  Floor bytes per level: HBM
+                 carries the index/offset/row streams and the dense optimizer
+                 pass; the array's own level (one XCD's L2, the memory-side
+                 cache, or HBM at 64-byte sector granularity) carries each
+                 distinct chunk of the batch once per gather and once per
+                 read-modify-write.  Peaks: 8 TB/s for HBM (vendor); streaming
+                 reads measured at start-up for the caches (no published
+                 figure), reported with the random 64-byte gather rates.
                  Events bracket the calls of every --event-every-th timed step
                  only: each event record costs the stream about 4 us, which
                  would otherwise be counted as step time.
@@ -81,17 +88,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def hbm_bytes(wl, B, N):
-    """Algorithmic HBM bytes of one forward and one backward launch.
+SECTOR = 64  # bytes a random access of a few bytes moves at HBM (one sector)
 
-    Forward: indices (8 B each) + offsets (8 B per bag + 1) + pooled output
-    (4 B per element).  Backward: the same index/offset stream + the output
-    gradient (4 B per element).  The gathered and deposited array traffic is
-    counted at the array's own level (L2/MALL when resident), not here.
-    """
-    stream = 8 * N + 8 * (wl.T * B + 1)
-    rows = 4 * B * wl.T * wl.d
-    return stream + rows, stream + rows
+
+def array_level(wl):
+    """Memory level the shared array lives in: one XCD's L2 (4 MiB), the
+    memory-side cache (256 MiB) or HBM."""
+    nbytes = wl.M * (2 if wl.weight_dtype == "bf16" else 4)
+    if nbytes <= 4 << 20:
+        return "l2"
+    if nbytes <= 256 << 20:
+        return "cache"
+    return "hbm"
 
 
 def optimizer_bytes(wl):
@@ -102,6 +110,58 @@ def optimizer_bytes(wl):
     wsz = 2 if wl.weight_dtype == "bf16" else 4
     state = 8 if wl.optimizer == "adagrad" else 0
     return wl.M * (4 + 4 + 2 * wsz + state)
+
+
+def distinct_chunks(wl, pss, hp, idx, off, dev):
+    """Distinct chunk bases of a batch, and distinct 64-byte sectors of the
+    array those chunks touch, from the library's export of every chunk base
+    (identical lookups share a base; on-chip aggregation moves each once)."""
+    import torch
+    bases = torch.empty((int(hp.num_indices), wl.C), dtype=torch.int32, device=dev)
+    pss.pss_debug_addresses(wl.M, wl.Z, wl.d, hp, idx, off, bases)
+    b = bases.view(-1).to(torch.int64) & 0xFFFFFFFF
+    del bases
+    uniq = torch.unique(b)
+    sw = 2 if wl.weight_dtype == "bf16" else 4
+    first = uniq * sw // SECTOR
+    last = (uniq * sw + wl.Z * sw - 1) // SECTOR  # a chunk may straddle a sector boundary
+    sectors = torch.unique(torch.cat([first, last])).numel()
+    return int(uniq.numel()), int(sectors)
+
+
+def traffic(wl, B, N, distinct):
+    """Floor bytes of one forward and one backward launch at each memory level.
+
+    HBM: indices (8 B each) + offsets (8 B per bag + 1) + pooled rows (4 B per
+    element) in each direction, and the dense optimizer pass when one runs.
+    Array level: identical lookups read and update the same chunk, so with
+    on-chip aggregation the forward must read each distinct chunk of the batch
+    once (Z weights) and the backward must read and write each once (Z
+    float32 values).  When the array lives in HBM those accesses are random
+    and move whole 64-byte sectors: each distinct sector is read by the
+    forward and read and written by the backward.
+    distinct = (distinct chunk bases, distinct sectors) of the batch.
+    Returns {level: (forward bytes, backward bytes)}.
+    """
+    sw = 2 if wl.weight_dtype == "bf16" else 4
+    chunks, sectors = distinct
+    stream = 8 * N + 8 * (wl.T * B + 1)
+    rows = 4 * B * wl.T * wl.d
+    fwd, bwd = stream + rows, stream + rows + optimizer_bytes(wl)
+    level = array_level(wl)
+    if level == "hbm":
+        return {"hbm": (fwd + sectors * SECTOR, bwd + 2 * sectors * SECTOR)}
+    return {"hbm": (fwd, bwd), level: (chunks * wl.Z * sw, 2 * chunks * wl.Z * 4)}
+
+
+def level_peaks(measured):
+    """GB/s per level: the vendor's HBM figure; measured streaming reads for
+    the caches, which have no published peak."""
+    peaks = {"hbm": (HBM_PEAK_GBS, "vendor")}
+    if measured:
+        peaks["cache"] = (measured["cache_read_gbs"], "measured streaming read")
+        peaks["l2"] = (measured["l2_read_gbs"], "measured streaming read")
+    return peaks
 
 
 def cpu_baseline(wl, x, a, b, budget_s=24.0):
@@ -139,9 +199,13 @@ def cpu_baseline(wl, x, a, b, budget_s=24.0):
             break
         Bp *= 2
     n, dt, Bp = best
-    return {"value": n / dt, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+    host = os.cpu_count()
+    avail = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else host
+    return {"value": n / dt, "unit": "lookups/s", "cores": 1, "host_cores": host,
+            "available_cores": avail, "kind": "oracle",
             "sample": f"first {Bp} of {x.B} samples of batch 0 ({n} lookups, all {wl.T} tables), "
-                      f"one forward+gradient+update pass, float64 NumPy, single thread"}
+                      f"one forward+gradient+update pass, float64 NumPy, single thread: "
+                      f"1 of {host} host cores ({avail} available to the process)"}
 
 
 def main():
@@ -154,6 +218,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prepare", action="store_true",
                     help="no pss_prepare_backward call: the backward groups the batch itself")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip measuring the L2 / memory-side cache / HBM denominators")
     ap.add_argument("--event-every", type=int, default=5,
                     help="time the calls of every n-th timed step with HIP events")
     args = ap.parse_args()
@@ -173,6 +239,13 @@ def main():
              "sorted": pss.PSS_BWD_SORTED, "sparse": pss.PSS_BWD_SPARSE}[args.variant]
     dt_code = pss.PSS_BF16 if wl.weight_dtype == "bf16" else pss.PSS_F32
 
+    measured = None
+    if not args.no_peaks:
+        from paper_2207_10731_amd import peaks
+        t0 = time.perf_counter()
+        measured = peaks.measure(dev)
+        log("[bench] measured peaks (GB/s): " + ", ".join(f"{k} {v:.0f}" for k, v in measured.items())
+            + f" in {time.perf_counter() - t0:.1f}s")
     t0 = time.perf_counter()
     xs = [synth.make_inputs(wl, batch=k) for k in range(ROTATE)]
     log(f"[bench] {wl.name}: inputs generated in {time.perf_counter() - t0:.1f}s; "
@@ -228,23 +301,46 @@ def main():
     ms_per_step = 1e3 * wall / args.steps
     N_avg = lookups / args.steps
 
-    fb, bb = hbm_bytes(wl, wl.B, N_avg)
-    ob = optimizer_bytes(wl)
     f_avg, b_avg = fwd_ms.mean() * 1e-3, bwd_ms.mean() * 1e-3
+    distinct = distinct_chunks(wl, pss, hps[0], idx[0], off[0], dev)
+    log(f"[bench] batch 0: {distinct[0]} distinct chunk bases of {xs[0].N * wl.C} chunks, "
+        f"{distinct[1]} distinct 64-byte sectors")
+    tr = traffic(wl, wl.B, N_avg, distinct)
+    peaks_gbs = level_peaks(measured)
+    t_step = wall / args.steps
+    levels = {}
+    for lv, (fb_l, bb_l) in tr.items():
+        pk = peaks_gbs.get(lv)
+        levels[lv] = {"bytes_per_step": fb_l + bb_l, "forward_bytes": fb_l, "backward_bytes": bb_l,
+                      "peak_gbs": None if pk is None else pk[0],
+                      "peak_source": None if pk is None else pk[1],
+                      "t_star_us": None if pk is None else (fb_l + bb_l) / (pk[0] * 1e9) * 1e6,
+                      "achieved_gbs": (fb_l + bb_l) / t_step / 1e9}
+    timed = {lv: v for lv, v in levels.items() if v["t_star_us"] is not None}
+    step_bound = max(timed, key=lambda lv: timed[lv]["t_star_us"])
+    t_star = timed[step_bound]["t_star_us"] * 1e-6
     # The roofline object describes the forward kernel: pss_forward launches
-    # exactly one kernel (so events around the call time that kernel), and it
-    # is the longest single kernel of the step.  The backward call launches
-    # the keygen, sort passes, reduction (and optimizer) kernels; its
+    # exactly one kernel (so events around the call time that kernel), the
+    # longest single kernel of the headline step.  Its bound is the level
+    # whose floor time is largest for the forward's own bytes.  The backward
+    # call launches the grouping, reduction (and optimizer) kernels; its
     # call-level figures are reported beside it.
-    dom, dom_bytes, dom_t = "forward_kernel", fb, f_avg
+    fwd_lv = max(timed, key=lambda lv: timed[lv]["forward_bytes"] / peaks_gbs[lv][0])
+    dom, dom_bytes, dom_t = "forward_kernel", tr[fwd_lv][0], f_avg
+    dom_peak = peaks_gbs[fwd_lv][0]
     achieved = dom_bytes / dom_t / 1e9
-    step_bytes = fb + bb + ob
-    t_star = step_bytes / (HBM_PEAK_GBS * 1e9)
+    fb, bb = tr["hbm"]
     log(f"[bench] forward   median {np.median(fwd_ms)*1e3:.1f} us  p10 {np.percentile(fwd_ms,10)*1e3:.1f}"
-        f"  p90 {np.percentile(fwd_ms,90)*1e3:.1f}  -> {fb/f_avg/1e9:.0f} GB/s (HBM algorithmic)")
+        f"  p90 {np.percentile(fwd_ms,90)*1e3:.1f}  -> {achieved:.0f} GB/s at level {fwd_lv}")
     log(f"[bench] backward  median {np.median(bwd_ms)*1e3:.1f} us  p10 {np.percentile(bwd_ms,10)*1e3:.1f}"
-        f"  p90 {np.percentile(bwd_ms,90)*1e3:.1f}  -> {(bb+ob)/b_avg/1e9:.0f} GB/s (HBM algorithmic)")
-    log(f"[bench] step {ms_per_step*1e3:.1f} us, T* {t_star*1e6:.1f} us, frac {t_star/(wall/args.steps):.3f}")
+        f"  p90 {np.percentile(bwd_ms,90)*1e3:.1f}  -> {bb/b_avg/1e9:.0f} GB/s (HBM floor bytes)")
+    for lv, v in levels.items():
+        tstar = "n/a" if v["t_star_us"] is None else f"{v['t_star_us']:.1f} us"
+        log(f"[bench] level {lv}: {v['bytes_per_step']/1e6:.1f} MB/step, peak "
+            f"{v['peak_gbs'] if v['peak_gbs'] is None else round(v['peak_gbs'])} GB/s "
+            f"({v['peak_source']}), T* {tstar}, achieved {v['achieved_gbs']:.0f} GB/s")
+    log(f"[bench] step {ms_per_step*1e3:.1f} us, T* {t_star*1e6:.1f} us ({step_bound}), "
+        f"frac {t_star/t_step:.3f}")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -271,16 +367,19 @@ def main():
                    "M": wl.M, "storage": wl.weight_dtype, "optimizer": wl.optimizer,
                    "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": not args.no_prepare,
                    "lookups_per_step": N_avg},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": counted_traffic(wl.name),
+        "roofline": {"bound": fwd_lv, "kernel": dom, "achieved": achieved, "peak": dom_peak,
+                     "unit": "GB/s", "frac": achieved / dom_peak,
+                     "traffic": counted_traffic(wl.name) if fwd_lv == "hbm" else None,
                      "bytes_per_launch": dom_bytes, "avg_launch_us": dom_t * 1e6,
                      "timed_launches": len(evs),
-                     "step_hbm_bytes": step_bytes, "step_t_star_us": t_star * 1e6,
-                     "step_frac": t_star / (wall / args.steps),
+                     "step_bound": step_bound, "step_t_star_us": t_star * 1e6,
+                     "step_frac": t_star / t_step,
+                     "step_hbm_bytes": fb + bb,
+                     "levels": levels, "measured_peaks_gbs": measured,
+                     "distinct_chunks_batch0": distinct[0], "distinct_sectors_batch0": distinct[1],
                      "forward_us": f_avg * 1e6, "backward_update_us": b_avg * 1e6,
-                     "backward_update_hbm_bytes": bb + ob,
-                     "backward_update_gbs": (bb + ob) / b_avg / 1e9},
+                     "backward_update_hbm_bytes": bb,
+                     "backward_update_gbs": bb / b_avg / 1e9},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -1,4 +1,5 @@
-"""Builds libpss.so (all HIP sources, gfx950) in place, next to this file.
+"""Builds libpss.so (the layer's HIP sources, gfx950) and libpss_bench.so
+(the measurement kernels) in place, next to this file.
 
 Usage:  python -m paper_2207_10731_amd.build   (or build() from Python)
 Each source is compiled in its own hipcc process, then linked; the library is
@@ -18,7 +19,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpss.so")
 SOURCES = ["pss_api.hip", "pss_forward.hip", "pss_backward.hip", "pss_sorted.hip",
-           "pss_sparse.hip", "pss_bench.hip"]
+           "pss_sparse.hip"]
+BENCH_LIB = os.path.join(PKG, "libpss_bench.so")
+BENCH_SOURCES = ["pss_bench.hip"]
 ARCH = "gfx950"
 
 CXXFLAGS = [
@@ -40,19 +43,25 @@ def _run(cmd):
     return res.stdout
 
 
+def _link(objs, lib):
+    tmp = lib + ".tmp"
+    out = _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    os.replace(tmp, lib)
+    return out
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
     cmds = []
-    for src in SOURCES:
+    objs = {}
+    for src in SOURCES + BENCH_SOURCES:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        objs.append(obj)
+        objs[src] = obj
         cmds.append([hipcc(), *CXXFLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(max_workers=min(len(cmds), 4)) as ex:
         outs = list(ex.map(_run, cmds))
-    tmp = LIB + ".tmp"
-    outs.append(_run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]))
-    os.replace(tmp, LIB)
+    outs.append(_link([objs[s] for s in SOURCES], LIB))
+    outs.append(_link([objs[s] for s in BENCH_SOURCES], BENCH_LIB))
     if verbose:
         for o in outs:
             if o.strip():

@@ -18,9 +18,7 @@ def main():
     ap.add_argument("--mib", type=int, default=1024)
     ap.add_argument("--reps", type=int, default=3)
     a = ap.parse_args()
-    lib = pss.load_library()
-    lib.pss_bench_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
-    lib.pss_bench_copy.restype = ctypes.c_int
+    lib = pss.load_bench_library()
     nbytes = a.mib << 20
     src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)

@@ -19,11 +19,41 @@ def lib():
 
 
 def test_exports_every_declared_function(lib):
-    names = pss.header_functions()
+    names = pss.header_functions([pss.HEADER])
     assert {"pss_forward", "pss_backward_update", "pss_debug_addresses",
             "pss_hash_params_from_seed", "pss_status_string"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
+
+
+def test_measurement_library_is_separate(lib):
+    """include/pss_bench.h is served by libpss_bench.so; the layer's library
+    exports none of it."""
+    import os
+    bench = pss.load_bench_library()
+    names = pss.header_functions([os.path.join(pss.INCLUDE, "pss_bench.h")])
+    assert {"pss_bench_copy", "pss_bench_read", "pss_bench_gather"} <= set(names)
+    for n in names:
+        assert hasattr(bench, n), n
+        assert not hasattr(lib, n), n
+    assert set(pss.header_functions()) == set(names) | set(pss.header_functions([pss.HEADER]))
+
+
+def test_flag_layout(lib):
+    """Backward variant in bits 0-1, options in bits 2-7; the sign field value
+    3 << 2 and any bit from 8 up are rejected before anything is enqueued."""
+    assert pss.PSS_BWD_MASK == 3
+    opts = [pss.PSS_SIGN_PM1, pss.PSS_SIGN_SPARSE, pss.PSS_POOL_MEAN, pss.PSS_INDEX_I32,
+            pss.PSS_ROWS_BF16, pss.PSS_PREPARE_BACKWARD]
+    for f in opts:
+        assert f & 3 == 0 and f < (1 << 8)
+    assert pss.PSS_SIGN_MASK == 3 << 2
+    hp = pss.make_hash_params(1, num_tables=1, batch=1, num_indices=1)
+    for bad in [pss.PSS_SIGN_MASK, 1 << 8, 1 << 31]:
+        hp.flags = bad
+        st = lib.pss_forward(ctypes.c_void_p(8), 4096, 4, 16, ctypes.byref(hp), ctypes.c_void_p(8),
+                             ctypes.c_void_p(8), ctypes.c_void_p(8), None)
+        assert st == pss.PSS_ERR_INVALID_ARG, bad
 
 
 def test_status_strings(lib):

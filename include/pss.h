@@ -115,8 +115,14 @@ enum {
   PSS_ERR_INVALID_ARG = 1,
   PSS_ERR_UNSUPPORTED = 2,
   PSS_ERR_HIP = 3,
-  PSS_ERR_NO_MEMORY = 4
+  PSS_ERR_NO_MEMORY = 4,
+  PSS_ERR_SCRATCH_LIMIT = 5  /* pss_backward_update_noalloc: more scratch needed
+                                than PSS_NOALLOC_SCRATCH_BYTES */
 };
+
+/* Bytes of the static device scratch of pss_backward_update_noalloc (each
+ * GPU the library runs on holds one such array until the process ends). */
+#define PSS_NOALLOC_SCRATCH_BYTES (64u << 20)
 
 /* Backward variant, bits 0-1 of pss_hash_params.flags.
  *   AUTO    library's choice for the shape: SPARSE when the update is not
@@ -222,6 +228,29 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
                         const pss_hash_params* hash_params, const void* indices,
                         const void* offsets, const void* grad_out, float lr,
                         hipStream_t stream);
+
+/* pss_backward_update for callers that cannot allocate memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, checks, variants and results, but every scratch buffer
+ * (the float32 gradient buffer of an unfused update, the SORTED grouping,
+ * the SPARSE workspace) lives in one static device array of
+ * PSS_NOALLOC_SCRATCH_BYTES per GPU, and the call makes no allocation of
+ * any kind (no hipMalloc, hipFree, pool or library allocation).  A call whose
+ * scratch would exceed that size returns PSS_ERR_SCRATCH_LIMIT before
+ * anything is enqueued: the SORTED grouping takes 16 B per lookup plus
+ * about 0.5 B per lookup of digit counts (the headline one-hot batch of 1.7M
+ * lookups needs 28 MB), an unfused update adds 4 B per weight of M.  A call
+ * neither uses nor drops a grouping prepared by pss_prepare_backward or
+ * PSS_PREPARE_BACKWARD.  Every call on one GPU shares that GPU's array and
+ * leaves its contents behind (each call clears what it reads before
+ * writing): calls that overlap in time on one GPU (different streams, or
+ * host threads without ordering) race on it and must be ordered by the
+ * caller.  The device address of the array is looked up on the first call
+ * on each device (with that device current). */
+int pss_backward_update_noalloc(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
+                                const pss_hash_params* hash_params, const void* indices,
+                                const void* offsets, const void* grad_out, float lr,
+                                hipStream_t stream);
 
 /* Sparse gradient of the shared array (paper Alg. 1, sparse branch:
  * findUnique over the read locations, scatter_add of the output gradient):

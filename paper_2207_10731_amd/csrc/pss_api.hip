@@ -425,6 +425,38 @@ hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state
   return e;
 }
 
+// ---------------------------------------------------------------------------
+// Scratch of pss_backward_update_noalloc: a static device array (each GPU
+// holds its own copy, from the library's first use on it until the process
+// ends).  In host code `scratch` names a host-side stand-in, not the device
+// memory: its device address is taken once per device with
+// hipGetSymbolAddress, with that device current, and only that address is
+// passed to kernels.
+// ---------------------------------------------------------------------------
+constexpr size_t kStaticScratchBytes = static_cast<size_t>(PSS_NOALLOC_SCRATCH_BYTES);
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+std::mutex g_static_mu;
+std::map<int, void*> g_static_ptr;  // device -> device address of `scratch`
+
+hipError_t static_scratch_for_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  auto it = g_static_ptr.find(dev);
+  if (it != g_static_ptr.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  void* ptr = nullptr;
+  e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || ptr == nullptr) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+  g_static_ptr[dev] = ptr;
+  *out = ptr;
+  return hipSuccess;
+}
+
 uint64_t splitmix64_next(uint64_t* state) {
   uint64_t z = (*state += 0x9E3779B97F4A7C15ull);
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -508,6 +540,24 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
                                         grad_out, lr, scratch.ptr(), prep, stream);
   const hipError_t ef = scratch.done();
   return (e != hipSuccess || ef != hipSuccess) ? PSS_ERR_HIP : PSS_OK;
+}
+
+int pss_backward_update_noalloc(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
+                                const pss_hash_params* hash_params, const void* indices,
+                                const void* offsets, const void* grad_out, float lr,
+                                hipStream_t stream) {
+  BackwardPlan plan;
+  const int st = plan_backward(shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr,
+                               &plan);
+  if (st != PSS_OK) return st == kNothingToDo ? PSS_OK : st;
+  if (plan.g_bytes + plan.ws_bytes > kStaticScratchBytes) return PSS_ERR_SCRATCH_LIMIT;
+  void* ws = nullptr;
+  if (plan.g_bytes + plan.ws_bytes > 0 && static_scratch_for_current_device(&ws) != hipSuccess)
+    return PSS_ERR_HIP;
+  return enqueue_backward(plan, shared, state, hash_params->eps, indices, offsets, grad_out, lr, ws,
+                          nullptr, stream) == hipSuccess
+             ? PSS_OK
+             : PSS_ERR_HIP;
 }
 
 int pss_gradient_sparse(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,
@@ -672,6 +722,8 @@ const char* pss_status_string(int status) {
     case PSS_ERR_UNSUPPORTED: return "unsupported argument combination";
     case PSS_ERR_HIP: return "HIP runtime or launch failure";
     case PSS_ERR_NO_MEMORY: return "out of device memory for scratch space";
+    case PSS_ERR_SCRATCH_LIMIT:
+      return "the call needs more scratch than the allocation-free entry point holds";
     default: return "unknown status";
   }
 }

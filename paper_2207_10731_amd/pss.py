@@ -22,6 +22,8 @@ HEADER = os.path.join(INCLUDE, "pss.h")
 PSS_PRIME = 2**31 - 1
 PSS_F32, PSS_BF16 = 0, 1
 PSS_OK, PSS_ERR_INVALID_ARG, PSS_ERR_UNSUPPORTED, PSS_ERR_HIP, PSS_ERR_NO_MEMORY = 0, 1, 2, 3, 4
+PSS_ERR_SCRATCH_LIMIT = 5
+PSS_NOALLOC_SCRATCH_BYTES = 64 << 20
 PSS_BWD_AUTO, PSS_BWD_ATOMIC, PSS_BWD_SORTED, PSS_BWD_SPARSE = 0, 1, 2, 3
 PSS_BWD_MASK = 3
 PSS_SIGN_PM1, PSS_SIGN_SPARSE, PSS_SIGN_MASK = 1 << 2, 2 << 2, 3 << 2
@@ -66,6 +68,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_hash_params_from_seed.argtypes = [u64, hp]
     lib.pss_forward.argtypes = [vp, i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_backward_update.argtypes = [vp, vp, i64, i32, i32, hp, vp, vp, vp, ctypes.c_float, vp]
+    lib.pss_backward_update_noalloc.argtypes = lib.pss_backward_update.argtypes
     lib.pss_prepare_backward.argtypes = [i64, i32, i32, hp, vp, vp, vp]
     lib.pss_debug_addresses.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
     lib.pss_debug_signs.argtypes = [i64, i32, i32, hp, vp, vp, vp, vp]
@@ -77,6 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_status_string.restype = ctypes.c_char_p
     lib.pss_release_scratch.argtypes = []
     for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
+                 "pss_backward_update_noalloc",
                  "pss_prepare_backward", "pss_debug_addresses", "pss_debug_signs",
                  "pss_gradient_sparse",
                  "pss_hash_bases_host", "pss_hash_signs_host", "pss_validate_offsets_host",
@@ -249,6 +253,14 @@ def pss_backward_update(shared, state, M, Z, d, hash_params, indices, offsets, g
                         stream=None):
     _backward("pss_backward_update", shared, state, M, Z, d, hash_params, indices, offsets,
               grad_out, lr, stream)
+
+
+def pss_backward_update_noalloc(shared, state, M, Z, d, hash_params, indices, offsets, grad_out,
+                                lr, stream=None):
+    """The allocation-free backward: scratch in the library's static device
+    array (PSS_ERR_SCRATCH_LIMIT when the call needs more)."""
+    _backward("pss_backward_update_noalloc", shared, state, M, Z, d, hash_params, indices,
+              offsets, grad_out, lr, stream)
 
 
 def _backward(name, shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr, stream):

@@ -57,7 +57,7 @@ def test_flag_layout(lib):
 
 
 def test_status_strings(lib):
-    for s in range(5):
+    for s in range(6):
         assert pss.status_string(s) and pss.status_string(s) != "unknown status"
     assert pss.status_string(99) == "unknown status"
 
@@ -252,3 +252,30 @@ def test_prepare_rejects_bad_arguments(lib):
     assert call(a=0) == pss.PSS_ERR_INVALID_ARG
     assert call(T=0) == pss.PSS_ERR_INVALID_ARG
     assert call(offsets=None) == pss.PSS_ERR_INVALID_ARG
+
+
+def test_noalloc_rejects_bad_arguments_and_oversized_calls(lib):
+    """The allocation-free backward runs the same host checks, and refuses a
+    call whose scratch exceeds its static array before anything is enqueued
+    (no GPU is touched: the pointers are never dereferenced)."""
+    dummy = ctypes.c_void_p(0x1000)
+    f = lib.pss_backward_update_noalloc
+    hp = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 0)
+    assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp), dummy, dummy, dummy,
+             ctypes.c_float(float("nan")), None) == pss.PSS_ERR_INVALID_ARG
+    assert f(None, None, 4096, 4, 16, ctypes.byref(hp), dummy, dummy, dummy,
+             ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
+    # SORTED grouping of 4.2M lookups: 16 B each, beyond 64 MiB
+    big = pss.pss_hash_params(5, 7, 26, 262144, 26 * 262144, 0, 1e-10, pss.PSS_BWD_SORTED)
+    assert f(dummy, None, 2_500_000, 32, 128, ctypes.byref(big), dummy, dummy, dummy,
+             ctypes.c_float(0.1), None) == pss.PSS_ERR_SCRATCH_LIMIT
+    # an unfused update needs a float32 gradient buffer of M: 64 MiB + 4 B is too much
+    hp_m = pss.pss_hash_params(5, 7, 1, 1, 1, 0, 1e-10, pss.PSS_BWD_ATOMIC)
+    M = (pss.PSS_NOALLOC_SCRATCH_BYTES // 4) + 1
+    assert f(dummy, dummy, M, 4, 16, ctypes.byref(hp_m), dummy, dummy, dummy,
+             ctypes.c_float(0.1), None) == pss.PSS_ERR_SCRATCH_LIMIT
+    assert "allocation-free" in pss.status_string(pss.PSS_ERR_SCRATCH_LIMIT)
+    # no lookups: nothing to do, whatever the size
+    hp0 = pss.pss_hash_params(5, 7, 26, 262144, 0, 0, 1e-10, 0)
+    assert f(dummy, None, 2_500_000, 32, 128, ctypes.byref(hp0), dummy, dummy, dummy,
+             ctypes.c_float(0.1), None) == pss.PSS_OK

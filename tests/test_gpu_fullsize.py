@@ -4,7 +4,15 @@ variant; the step as the bench runs it, with PSS_PREPARE_BACKWARD on the
 forward, for the one-hot and multi-hot workloads), checked on sampled
 outputs the oracle evaluates one by one: pooled rows of sampled bags
 (forward_at) and updated weights at sampled elements of the shared array
-(gradient_at), half of them elements that the batch reads."""
+(gradient_at), half of them elements that the batch reads.
+
+Alg. 1's sparse branch at full size as well: the SPARSE backward variant on
+every workload (sampled elements, as above), and the exported sparse
+gradient (pss_gradient_sparse) on the workloads whose arrays fit the export:
+its location count equals the number of distinct elements the batch reads
+(the union of the oracle's chunk windows), its locations ascend strictly,
+every sampled element the batch reads is listed with the oracle's value, and
+no sampled element it does not read is listed."""
 import numpy as np
 import pytest
 import torch
@@ -149,3 +157,60 @@ def _check_backward(F, grad):
         assert np.array_equal(w_gpu[untouched], w_old[untouched])
     else:
         assert np.array_equal(w_gpu[untouched].view(np.uint32), w_old[untouched].view(np.uint32))
+
+
+@pytest.mark.parametrize("key", FULL)
+def test_fullsize_sparse_backward_sampled_elements(key):
+    F = Full(key, flags=pss.PSS_BWD_SPARSE)
+    wl = F.wl
+    g, grad = _grad(F)
+    print(f"full-size {key}: SPARSE backward over {F.x.N} lookups", flush=True)
+    pss.pss_backward_update(F.shared, F.state, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, wl.lr)
+    torch.cuda.synchronize()
+    del g
+    _check_backward(F, grad)
+
+
+def _distinct_elements(F):
+    """Elements read by the batch: the union of the windows [h, h + Z) mod M
+    of the oracle's distinct chunk bases, counted with a difference array."""
+    wl = F.wl
+    bases = np.unique(o.chunk_bases(wl.M, wl.Z, wl.d, wl.T, wl.B, F.a, F.b, F.x.indices,
+                                    F.x.offsets).ravel()).astype(np.int64)
+    diff = np.zeros(wl.M + 1, dtype=np.int64)
+    end = bases + wl.Z
+    np.add.at(diff, bases, 1)
+    np.add.at(diff, np.minimum(end, wl.M), -1)
+    wrap = end > wl.M  # windows running past the end continue at 0
+    np.add.at(diff, np.zeros(int(wrap.sum()), dtype=np.int64), 1)
+    np.add.at(diff, end[wrap] - wl.M, -1)
+    return int((np.cumsum(diff[:-1]) > 0).sum())
+
+
+@pytest.mark.parametrize("key", ["c2", "c3", "c5"])
+def test_fullsize_gradient_sparse(key):
+    F = Full(key)
+    wl = F.wl
+    g, grad = _grad(F)
+    cap = min(wl.M, F.x.N * wl.d)
+    loc = torch.empty(cap, dtype=torch.int32, device=F.dev)
+    val = torch.empty(cap, dtype=torch.float32, device=F.dev)
+    nu = torch.zeros(1, dtype=torch.int64, device=F.dev)
+    print(f"full-size {key}: sparse gradient over {F.x.N} lookups", flush=True)
+    pss.pss_gradient_sparse(wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, loc, val, nu)
+    torch.cuda.synchronize()
+    del g
+    U = int(nu.item())
+    assert U == _distinct_elements(F)
+    locs = loc[:U].cpu().numpy().view(np.uint32).astype(np.int64)
+    vals = val[:U].cpu().numpy().astype(np.float64)
+    assert np.all(np.diff(locs) > 0) and locs[0] >= 0 and locs[-1] < wl.M
+    where = _sample_elements(F, np.random.default_rng(300))
+    G, A, cnt = o.gradient_at(wl.M, wl.Z, wl.d, wl.T, wl.B, F.a, F.b, F.x.indices, F.x.offsets,
+                              grad, where)
+    pos = np.searchsorted(locs, where)
+    listed = (pos < U) & (locs[np.minimum(pos, U - 1)] == where)
+    assert np.array_equal(listed, cnt > 0)
+    got = vals[pos[listed]]
+    err = np.abs(got - G[listed])
+    assert np.all(err <= 1e-5 * A[listed] + 1e-30), f"{(err > 1e-5 * A[listed]).sum()} values off"

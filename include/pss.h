@@ -43,6 +43,17 @@
  *   PSS_INDEX_I32  indices and offsets are int32.
  *   PSS_ROWS_BF16  out is written, and grad_out read, as bfloat16 (out is
  *     rounded to nearest even from the float32 result).
+ *   PSS_DEPOSIT_BY_ADDRESS  with the SORTED variant (or AUTO): every (lookup,
+ *     dim) contribution becomes an (address, value) record, the records are
+ *     radix-sorted by address tile (2^14 elements) and each tile's records
+ *     are summed on chip and applied to the array (or the float32 gradient
+ *     buffer) in one pass: no float atomics to memory, at the cost of 16 B
+ *     of scratch per (lookup, dim).  Requires N * d < 2^31 (else
+ *     PSS_ERR_UNSUPPORTED); invalid with ATOMIC or SPARSE
+ *     (PSS_ERR_UNSUPPORTED).  AUTO takes it by itself for chunks shorter than
+ *     a 64-byte memory line (Z < 16) on an array beyond the memory-side cache
+ *     (M * 4 > 256 MiB), where lookups seldom repeat and each contribution
+ *     would otherwise be an atomic to its own line.
  *   PSS_PREPARE_BACKWARD  read by pss_forward only (the other calls ignore
  *     it; pss_prepare_backward does the same work as a call of its own): the
  *     forward also groups the batch's lookups by token for the backward, on
@@ -127,7 +138,9 @@ enum {
 /* Backward variant, bits 0-1 of pss_hash_params.flags.
  *   AUTO    library's choice for the shape: SPARSE when the update is not
  *           fused (Adagrad, or bfloat16 storage) and M > 16 * N * d (low
- *           compression: a pass over all of M would dominate), else SORTED.
+ *           compression: a pass over all of M would dominate), else SORTED
+ *           (by address for short chunks on an array held in HBM, see
+ *           PSS_DEPOSIT_BY_ADDRESS).
  *   ATOMIC  every (lookup, dim) contribution added with a float atomic, into
  *           `shared` (SGD on float32 storage) or into a float32 gradient
  *           buffer followed by one streaming optimizer pass.
@@ -145,7 +158,7 @@ enum {
 enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2, PSS_BWD_SPARSE = 3 };
 #define PSS_BWD_MASK 3u
 
-/* Options, bits 2-7 of pss_hash_params.flags (see "Options" above). */
+/* Options, bits 2-8 of pss_hash_params.flags (see "Options" above). */
 #define PSS_SIGN_PM1 (1u << 2)
 #define PSS_SIGN_SPARSE (2u << 2)
 #define PSS_SIGN_MASK (3u << 2)
@@ -153,7 +166,10 @@ enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2, PSS_BWD_SPARSE 
 #define PSS_INDEX_I32 (1u << 5)
 #define PSS_ROWS_BF16 (1u << 6)
 #define PSS_PREPARE_BACKWARD (1u << 7)
-#define PSS_FLAGS_ALL 0xffu
+/* Bit 8: the deposit of the SORTED variant (or of AUTO) is ordered by
+ * address instead of grouped by token (see PSS_DEPOSIT_BY_ADDRESS above). */
+#define PSS_DEPOSIT_BY_ADDRESS (1u << 8)
+#define PSS_FLAGS_ALL 0x1ffu
 
 typedef struct {
   uint32_t a;            /* hash multiplier, 1 <= a <= p - 1 */
@@ -163,8 +179,8 @@ typedef struct {
   int64_t num_indices;   /* N = number of entries of `indices` (= offsets[T*B]) */
   int32_t weight_dtype;  /* pss_dtype of `shared` */
   float eps;             /* Adagrad epsilon (ignored by SGD); >= 0 */
-  uint32_t flags;        /* PSS_BWD_* in bits 0-1, options in bits 2-7; the
-                            sign field value 3 << 2 and bits 8 and up are
+  uint32_t flags;        /* PSS_BWD_* in bits 0-1, options in bits 2-8; the
+                            sign field value 3 << 2 and bits 9 and up are
                             invalid */
   uint32_t sign_a;       /* sign hash multiplier, 1 <= sign_a <= p - 1
                             (read only when a sign option is set) */

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpss.so")
 SOURCES = ["pss_api.hip", "pss_forward.hip", "pss_backward.hip", "pss_sorted.hip",
-           "pss_sparse.hip"]
+           "pss_sparse.hip", "pss_addr.hip"]
 BENCH_LIB = os.path.join(PKG, "libpss_bench.so")
 BENCH_SOURCES = ["pss_bench.hip"]
 ARCH = "gfx950"

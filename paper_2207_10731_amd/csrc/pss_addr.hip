@@ -1,0 +1,243 @@
+// Address-sorted deposit: Alg. 1's scatter_add with the contributions
+// ordered by address instead of added with atomics.
+//
+// Made for the regime where lookups rarely repeat and a chunk is shorter
+// than a memory line (the per-element hashing trick on an array held in HBM):
+// grouping by token then removes nothing, and every contribution would be a
+// float atomic to a different line, carried out at the memory side.  Here
+// each contribution becomes a record and each tile of the array is written
+// once:
+//
+//   records  item e, dim c -> (address (h(i, j) + k) mod M, scale * s * grad),
+//            at position e*d + c (the gradient rows are read in bag order);
+//            a chunk of factor 0 gives -0.0, which changes nothing
+//   sort     LSD radix sort of the records by address tile (the address bits
+//            from kAddrTileShift up; 8-bit digits, stable)
+//   starts   first record of every tile, from the sorted addresses
+//   apply    one workgroup per tile of 2^kAddrTileShift elements: the tile's
+//            records are summed into an LDS copy of the tile (LDS float
+//            atomics, initialised to -0.0 so that an element without records
+//            keeps its bits), then the tile is added to dst in one streaming
+//            pass (fused SGD) or stored as the tile of a float32 gradient
+//            buffer (every element of it, so the buffer needs no zero-fill).
+#include "pss_launch.hpp"
+
+namespace pss {
+
+constexpr uint32_t kAddrTile = 1u << kAddrTileShift;  // elements per tile
+constexpr int kApplyThreads = 512;
+
+// Records of the items of one 64-bag tile (one wavefront): lanes over the
+// dims (c = lane + 64 s), U items' gradient rows requested before any of
+// their records is written.
+template <int EPL, int U, bool SIGN, typename GT>
+__global__ __launch_bounds__(kBlockThreads) void addr_records_kernel(
+    const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
+    const GT* __restrict__ grad, const float scale, uint32_t* __restrict__ keys,
+    uint32_t* __restrict__ vals) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+  const uint64_t g0 = wave * kTileBags;
+  if (g0 >= p.num_bags) return;
+  const Tile tl = load_tile(p, offsets, g0, lane);
+  // pooled row r = b*T + t of bag g0 + lane
+  const uint64_t g = g0 + static_cast<uint64_t>(lane < tl.nb ? lane : 0);
+  const uint32_t t = static_cast<uint32_t>(g / p.B);
+  const uint32_t rr = static_cast<uint32_t>(g - static_cast<uint64_t>(t) * p.B) * p.T + t;
+
+  uint32_t step[EPL], step2[EPL], kk[EPL], cc[EPL];
+  bool act[EPL];
+#pragma unroll
+  for (int s = 0; s < EPL; ++s) {
+    const uint32_t c = static_cast<uint32_t>(lane) + kWave * s;
+    act[s] = c < p.d;
+    cc[s] = act[s] ? c : 0u;
+    const uint32_t j = cc[s] / p.Z;
+    kk[s] = cc[s] - j * p.Z;
+    step[s] = chunk_step(p.a, j);
+    step2[s] = SIGN ? chunk_step(p.a2, j) : 0u;
+  }
+
+  for (int64_t blk = tl.E0; blk < tl.E1; blk += kWave) {
+    const int64_t rem = tl.E1 - blk;
+    const int n = rem < kWave ? static_cast<int>(rem) : kWave;
+    const int64_t e = blk + lane;
+    const int bag = bag_of_item(tl, e);
+    const uint32_t tC = __shfl(tl.tC, bag);
+    const uint32_t r_l = __shfl(rr, bag);
+    uint32_t h0 = 0;
+    if (lane < n) h0 = item_hash(load_index(indices, e, p.idx32), tC, p.TC, p.a, p.b);
+    float il_l = 1.f;
+    if (p.mean) {
+      const uint32_t len = __shfl(tl.len, bag);
+      il_l = len ? 1.f / static_cast<float>(len) : 1.f;
+    }
+    for (int q0 = 0; q0 < n; q0 += U) {
+      float x[U][EPL];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = q0 + u < n ? q0 + u : n - 1;  // past the end: repeat the last item
+        const GT* row = grad + static_cast<uint64_t>(readlane_u32(r_l, q)) * p.d;
+#pragma unroll
+        for (int s = 0; s < EPL; ++s) x[u][s] = load_row(row, cc[s]);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (q0 + u >= n) break;
+        const int q = q0 + u;
+        const uint32_t h = readlane_u32(h0, q);
+        const float f = scale * (p.mean ? __builtin_bit_cast(float, readlane_u32(
+                                                                  __builtin_bit_cast(uint32_t, il_l), q))
+                                        : 1.f);
+        const uint32_t h20 = SIGN ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
+        const uint64_t rec = static_cast<uint64_t>(blk + q) * p.d;
+#pragma unroll
+        for (int s = 0; s < EPL; ++s) {
+          if (!act[s]) continue;
+          const uint32_t ent =
+              chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[s]), p.fm_c, p.M), add_mod_p(h20, step2[s]), p);
+          const Elem el = elem_of<SIGN>(ent, kk[s], p.M);
+          float v = f * x[u][s];
+          if (SIGN) v = el.read ? __uint_as_float(__float_as_uint(v) ^ el.neg) : -0.f;
+          keys[rec + cc[s]] = el.m;
+          vals[rec + cc[s]] = __float_as_uint(v);
+        }
+      }
+    }
+  }
+}
+
+// starts[x] = first record of tile x (records sorted by tile), for x in
+// [0, ntiles]; starts[ntiles] = n.  Position i writes the starts of the
+// tiles after the one of record i - 1 up to its own, so every entry is
+// written exactly once.
+__global__ __launch_bounds__(kBlockThreads) void addr_starts_kernel(const uint32_t* __restrict__ keys,
+                                                                    const uint32_t n, const uint32_t ntiles,
+                                                                    uint32_t* __restrict__ starts) {
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlockThreads;
+  for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i <= n;
+       i += stride) {
+    uint32_t tile = ntiles;
+    if (i < n) {
+      tile = keys[i] >> kAddrTileShift;
+      if (tile > ntiles - 1) tile = ntiles - 1;  // addresses are below M; guards memory anyway
+    }
+    int64_t prev = -1;
+    if (i > 0) {
+      uint32_t tp = keys[i - 1] >> kAddrTileShift;
+      prev = tp > ntiles - 1 ? ntiles - 1 : tp;
+    }
+    for (int64_t x = prev + 1; x <= static_cast<int64_t>(tile); ++x)
+      starts[x] = static_cast<uint32_t>(i);
+  }
+}
+
+// One workgroup per tile of the array: sum the tile's records in LDS, then
+// apply the tile to dst once.
+__global__ __launch_bounds__(kApplyThreads) void addr_apply_kernel(
+    float* __restrict__ dst, const uint32_t assign, const uint32_t M,
+    const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
+    const uint32_t* __restrict__ starts) {
+  __shared__ float tile[kAddrTile];
+  const uint32_t x = blockIdx.x;
+  const uint64_t base = static_cast<uint64_t>(x) << kAddrTileShift;
+  const uint32_t len = M - base < kAddrTile ? static_cast<uint32_t>(M - base) : kAddrTile;
+  for (uint32_t i = threadIdx.x; i < kAddrTile; i += kApplyThreads) tile[i] = -0.f;
+  __syncthreads();
+  const uint32_t lo = starts[x], hi = starts[x + 1];
+  for (uint32_t r = lo + threadIdx.x; r < hi; r += kApplyThreads)
+    atomicAdd(&tile[keys[r] & (kAddrTile - 1)], __uint_as_float(vals[r]));
+  __syncthreads();
+  float* out = dst + base;
+  if (len == kAddrTile) {
+    float4* o4 = reinterpret_cast<float4*>(out);
+    const float4* t4 = reinterpret_cast<const float4*>(tile);
+    for (uint32_t i = threadIdx.x; i < kAddrTile / 4; i += kApplyThreads) {
+      float4 v = t4[i];
+      if (!assign) {
+        const float4 w = o4[i];
+        v = make_float4(w.x + v.x, w.y + v.y, w.z + v.z, w.w + v.w);
+      }
+      o4[i] = v;
+    }
+  } else {
+    for (uint32_t i = threadIdx.x; i < len; i += kApplyThreads) out[i] = assign ? tile[i] : out[i] + tile[i];
+  }
+}
+
+static uint32_t addr_tiles(const KParams& p) {
+  return static_cast<uint32_t>((static_cast<uint64_t>(p.M) + kAddrTile - 1) >> kAddrTileShift);
+}
+
+size_t addr_workspace_bytes(const KParams& p) {
+  const uint64_t n = static_cast<uint64_t>(p.N) * p.d;
+  return n * 16 + radix_scratch_bytes(static_cast<int64_t>(n)) +
+         (static_cast<size_t>(addr_tiles(p)) + 1) * 4 + 256;
+}
+
+template <int EPL, int U, bool SIGN, typename GT>
+static void launch_records_t(const KParams& p, const void* indices, const void* offsets,
+                             const GT* grad, float scale, uint32_t* keys, uint32_t* vals,
+                             hipStream_t stream) {
+  const uint64_t tiles = (p.num_bags + kTileBags - 1) / kTileBags;
+  const uint64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  hipLaunchKernelGGL((addr_records_kernel<EPL, U, SIGN, GT>), dim3(static_cast<uint32_t>(blocks)),
+                     dim3(kBlockThreads), 0, stream, p, indices, offsets, grad, scale, keys, vals);
+}
+
+template <bool SIGN, typename GT>
+static void launch_records_s(const KParams& p, const void* indices, const void* offsets,
+                             const GT* grad, float scale, uint32_t* keys, uint32_t* vals,
+                             hipStream_t stream) {
+  if (p.d <= 64) return launch_records_t<1, 8, SIGN>(p, indices, offsets, grad, scale, keys, vals, stream);
+  if (p.d <= 128) return launch_records_t<2, 8, SIGN>(p, indices, offsets, grad, scale, keys, vals, stream);
+  if (p.d <= 256) return launch_records_t<4, 4, SIGN>(p, indices, offsets, grad, scale, keys, vals, stream);
+  if (p.d <= 1024) return launch_records_t<16, 1, SIGN>(p, indices, offsets, grad, scale, keys, vals, stream);
+  return launch_records_t<64, 1, SIGN>(p, indices, offsets, grad, scale, keys, vals, stream);
+}
+
+template <typename GT>
+static void launch_records_g(const KParams& p, const void* indices, const void* offsets,
+                             const GT* grad, float scale, uint32_t* keys, uint32_t* vals,
+                             hipStream_t stream) {
+  if (p.sign_mode) return launch_records_s<true>(p, indices, offsets, grad, scale, keys, vals, stream);
+  return launch_records_s<false>(p, indices, offsets, grad, scale, keys, vals, stream);
+}
+
+hipError_t launch_deposit_addr(float* dst, bool assign, float scale, const KParams& p,
+                               const void* indices, const void* offsets, const void* grad,
+                               void* workspace, hipStream_t stream) {
+  const uint64_t n = static_cast<uint64_t>(p.N) * p.d;
+  if (n >= (1ull << 31)) return hipErrorInvalidValue;
+  const uint32_t ntiles = addr_tiles(p);
+  uint32_t* k0 = static_cast<uint32_t*>(workspace);
+  uint32_t* v0 = k0 + n;
+  uint32_t* k1 = v0 + n;
+  uint32_t* v1 = k1 + n;
+  uint32_t* scratch = v1 + n;
+  uint32_t* starts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(scratch) +
+                                                 radix_scratch_bytes(static_cast<int64_t>(n)));
+  if (n > 0) {
+    if (p.rows_bf16)
+      launch_records_g(p, indices, offsets, static_cast<const uint16_t*>(grad), scale, k0, v0, stream);
+    else
+      launch_records_g(p, indices, offsets, static_cast<const float*>(grad), scale, k0, v0, stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // tile bits of the addresses (0 when the whole array is one tile)
+    int bits = 0;
+    while ((1ull << bits) < ntiles) ++bits;
+    e = radix_sort_pairs(k0, v0, k1, v1, static_cast<int64_t>(n), bits, scratch, stream, nullptr,
+                         false, kAddrTileShift);
+    if (e != hipSuccess) return e;
+  }
+  const uint64_t want = (n + 1 + kBlockThreads - 1) / kBlockThreads;
+  const uint32_t sgrid = static_cast<uint32_t>(want < 8192 ? want : 8192);
+  hipLaunchKernelGGL(addr_starts_kernel, dim3(sgrid), dim3(kBlockThreads), 0, stream, k0,
+                     static_cast<uint32_t>(n), ntiles, starts);
+  hipLaunchKernelGGL(addr_apply_kernel, dim3(ntiles), dim3(kApplyThreads), 0, stream, dst,
+                     assign ? 1u : 0u, p.M, k0, v0, starts);
+  return hipGetLastError();
+}
+
+}  // namespace pss

@@ -102,6 +102,16 @@ uint32_t auto_variant(int64_t M, const KParams& p, bool unfused, bool sparse_fit
   return PSS_BWD_SORTED;
 }
 
+// AUTO's deposit order for the SORTED variant: by address when a chunk is
+// shorter than a 64-byte memory line and the array lies beyond the
+// memory-side cache (M * 4 > 256 MiB).  There lookups seldom repeat, so
+// grouping by token removes nothing, and each contribution would be a float
+// atomic to its own line.  Needs N * d < 2^31 records.
+bool by_address_auto(int64_t M, const KParams& p) {
+  return p.Z * sizeof(float) < 64 && M * static_cast<int64_t>(sizeof(float)) > (256ll << 20) &&
+         p.N * static_cast<int64_t>(p.d) < (1ll << 31);
+}
+
 hipError_t pool_for_current_device(hipMemPool_t* out) {
   int dev = 0;
   hipError_t st = hipGetDevice(&dev);
@@ -348,10 +358,21 @@ Prepared* take_prepared(hipStream_t stream, const void* indices, const void* off
 
 int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; }
 
+// Whether a backward with these flags can run the SORTED variant grouped by
+// token (the grouping that pss_prepare_backward makes ahead): AUTO or SORTED,
+// not sorted by address (asked for, or AUTO's choice for the shape).
+bool groups_by_token(int64_t M, const KParams& p, const pss_hash_params* hp) {
+  const uint32_t variant = hp->flags & PSS_BWD_MASK;
+  if (variant != PSS_BWD_AUTO && variant != PSS_BWD_SORTED) return false;
+  if (hp->flags & PSS_DEPOSIT_BY_ADDRESS) return false;
+  return !(variant == PSS_BWD_AUTO && by_address_auto(M, p));
+}
+
 // One backward call: the variant that runs and the scratch it needs.
 struct BackwardPlan {
   KParams p;
   uint32_t variant = PSS_BWD_SORTED;  // ATOMIC, SORTED or SPARSE
+  bool by_address = false;            // SORTED: records sorted by address tile
   bool bf16 = false;
   bool fused = false;   // SGD on float32 storage: deposits go into `shared`
   size_t g_bytes = 0;   // float32 gradient buffer (unfused updates), 256-aligned
@@ -375,10 +396,16 @@ int plan_backward(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
   plan->bf16 = hp->weight_dtype == PSS_BF16;
   const bool sparse_fits = p.N * static_cast<int64_t>(p.C) < (1ll << 31);
   uint32_t variant = hp->flags & PSS_BWD_MASK;
+  const bool addr_asked = (hp->flags & PSS_DEPOSIT_BY_ADDRESS) != 0;
   if (variant == PSS_BWD_SPARSE && !sparse_fits) return PSS_ERR_UNSUPPORTED;
+  if (addr_asked && (variant == PSS_BWD_ATOMIC || variant == PSS_BWD_SPARSE))
+    return PSS_ERR_UNSUPPORTED;
+  if (addr_asked && p.N * static_cast<int64_t>(p.d) >= (1ll << 31)) return PSS_ERR_UNSUPPORTED;
   if (p.N == 0) return kNothingToDo;
-  if (variant == PSS_BWD_AUTO) variant = auto_variant(M, p, state != nullptr || plan->bf16, sparse_fits);
+  const bool auto_pick = variant == PSS_BWD_AUTO;
+  if (auto_pick) variant = auto_variant(M, p, state != nullptr || plan->bf16, sparse_fits);
   plan->variant = variant;
+  plan->by_address = variant == PSS_BWD_SORTED && (addr_asked || (auto_pick && by_address_auto(M, p)));
   if (variant == PSS_BWD_SPARSE) {
     // Alg. 1 sparse branch: 256 bytes for the unique count, then its workspace
     plan->ws_bytes = 256 + pss::sparse_workspace_bytes(p);
@@ -388,7 +415,9 @@ int plan_backward(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
   // the shared array.  Otherwise deposit G into a scratch buffer first.
   plan->fused = state == nullptr && !plan->bf16;
   plan->g_bytes = plan->fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
-  plan->ws_bytes = variant == PSS_BWD_SORTED ? pss::sorted_workspace_bytes(p) : 0;
+  plan->ws_bytes = variant != PSS_BWD_SORTED ? 0
+                   : plan->by_address       ? pss::addr_workspace_bytes(p)
+                                            : pss::sorted_workspace_bytes(p);
   return PSS_OK;
 }
 
@@ -410,6 +439,14 @@ hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state
   const float scale = plan.fused ? -lr : 1.f;
   const int64_t M = p.M;
   hipError_t e = hipSuccess;
+  if (plan.by_address) {
+    // every tile of G is stored whole: no zero-fill
+    e = pss::launch_deposit_addr(dst, !plan.fused, scale, p, indices, offsets, grad_out, sort_ws,
+                                 stream);
+    if (e == hipSuccess && !plan.fused)
+      e = pss::launch_optimizer(shared, plan.bf16, state, dst, M, lr, eps, stream);
+    return e;
+  }
   if (!plan.fused) e = pss::launch_zero(dst, M, stream);
   if (e == hipSuccess && prep != nullptr) {
     // the grouping ran on the library stream during the forward
@@ -490,14 +527,13 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
   if (shared == nullptr || offsets == nullptr || out == nullptr) return PSS_ERR_INVALID_ARG;
   if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
   const KParams p = make_params(M, Z, d, hash_params);
-  // The grouping is only reused by the SORTED backward (AUTO's choice when
-  // the update is fused), and only outside graph capture.
-  const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
-  // The preparation only saves the backward some work: if it cannot be set
+  // The grouping is only reused by the SORTED backward grouped by token
+  // (AUTO's usual choice when the update is fused), and only outside graph
+  // capture.  The preparation only saves the backward some work: if it cannot be set
   // up (no memory for its buffer, a failed runtime call), the forward runs
   // anyway and the backward groups the batch itself.
-  if ((hash_params->flags & PSS_PREPARE_BACKWARD) && p.N > 0 &&
-      (variant == PSS_BWD_AUTO || variant == PSS_BWD_SORTED) && !capturing(stream)) {
+  if ((hash_params->flags & PSS_PREPARE_BACKWARD) && p.N > 0 && groups_by_token(M, p, hash_params) &&
+      !capturing(stream)) {
     if (prepare_backward(p, indices, offsets, stream) != PSS_OK) (void)hipGetLastError();
   }
   return hip_status(pss::launch_forward(shared, hash_params->weight_dtype == PSS_BF16, p, indices,
@@ -511,9 +547,7 @@ int pss_prepare_backward(int64_t M, int32_t Z, int32_t d, const pss_hash_params*
   if (offsets == nullptr) return PSS_ERR_INVALID_ARG;
   if (indices == nullptr && hash_params->num_indices > 0) return PSS_ERR_INVALID_ARG;
   const KParams p = make_params(M, Z, d, hash_params);
-  const uint32_t variant = hash_params->flags & PSS_BWD_MASK;
-  if (p.N == 0 || (variant != PSS_BWD_AUTO && variant != PSS_BWD_SORTED) || capturing(stream))
-    return PSS_OK;
+  if (p.N == 0 || !groups_by_token(M, p, hash_params) || capturing(stream)) return PSS_OK;
   const int ps = prepare_backward(p, indices, offsets, stream);
   if (ps != PSS_OK) (void)hipGetLastError();
   return ps;
@@ -529,7 +563,9 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (st != PSS_OK) return st == kNothingToDo ? PSS_OK : st;
   std::unique_lock<std::mutex> prep_lock;
   Prepared* prep = take_prepared(stream, indices, offsets, plan.p,
-                                 plan.variant == PSS_BWD_SORTED && !capturing(stream), &prep_lock);
+                                 plan.variant == PSS_BWD_SORTED && !plan.by_address &&
+                                     !capturing(stream),
+                                 &prep_lock);
   if (prep != nullptr) plan.ws_bytes = 0;  // the grouping is already made
   CallScratch scratch;
   if (plan.g_bytes + plan.ws_bytes > 0) {

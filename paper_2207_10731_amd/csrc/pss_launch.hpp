@@ -44,16 +44,17 @@ hipError_t launch_reduce_sorted(float* dst, float scale, const KParams& p, const
 // with mean pooling also inv_len[b*T + t] = 1 / |bag| (nonempty bags).
 hipError_t launch_keygen(const KParams& p, const void* indices, const void* offsets,
                          uint32_t* keys, uint32_t* rows, float* inv_len, hipStream_t stream);
-// Stable LSD radix sort of (keys, vals) by the low `bits` bits (8-bit
-// digits); on return keys/vals point at whichever buffer pair holds the
-// result.  scratch: radix_scratch_bytes(n) bytes.  With n_dev the number of
+// Stable LSD radix sort of (keys, vals) by the `bits` bits from bit shift0
+// up (8-bit digits); on return keys/vals point at whichever buffer pair holds
+// the result.  scratch: radix_scratch_bytes(n) bytes.  With n_dev the number of
 // pairs is min(n, *n_dev) (read on the device; n sizes the launch).  With
 // first_counted the first pass's per-tile digit counts are already at the
 // start of scratch (written while the keys were made).
 size_t radix_scratch_bytes(int64_t n);
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
                             int64_t n, int bits, uint32_t* scratch, hipStream_t stream,
-                            const uint32_t* n_dev = nullptr, bool first_counted = false);
+                            const uint32_t* n_dev = nullptr, bool first_counted = false,
+                            int shift0 = 0);
 // Bits of the item hash the grouping sort orders for N lookups.
 int grouping_bits(int64_t N);
 
@@ -72,6 +73,18 @@ hipError_t launch_store_count(const uint32_t* total, int64_t* out, hipStream_t s
 hipError_t launch_sparse_update(const KParams& p, const void* indices, const void* offsets,
                                 const void* grad, void* workspace, uint32_t* num_unique32, void* w,
                                 bool bf16, float* state, float lr, float eps, hipStream_t stream);
+
+// Address-sorted deposit: every (lookup, dim) contribution becomes a record
+// (address, scale * value), the records are radix-sorted by address tile
+// (2^kAddrTileShift elements), each tile's records are summed in LDS and the
+// tile is applied once: added to dst (fused SGD) or stored as the tile of a
+// float32 gradient buffer dst of M elements (assign; no zero-fill needed).
+// Requires p.N * p.d < 2^31.  workspace: addr_workspace_bytes(p) bytes.
+constexpr int kAddrTileShift = 14;
+size_t addr_workspace_bytes(const KParams& p);
+hipError_t launch_deposit_addr(float* dst, bool assign, float scale, const KParams& p,
+                               const void* indices, const void* offsets, const void* grad,
+                               void* workspace, hipStream_t stream);
 
 // Dense optimizer pass over the M elements of a gradient buffer G (G[m] == 0
 // leaves element m untouched).  state == nullptr selects SGD.

@@ -698,7 +698,7 @@ size_t sorted_workspace_bytes(const KParams& p) {
 
 hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, uint32_t* vtmp,
                             int64_t n, int bits, uint32_t* scratch, hipStream_t stream,
-                            const uint32_t* n_dev, bool first_counted) {
+                            const uint32_t* n_dev, bool first_counted, int shift0) {
   if (n == 0) return hipSuccess;
   const uint32_t nblocks = static_cast<uint32_t>((n + kSortTile - 1) / kSortTile);
   // live keys counted on the device fill a prefix of the tiles: numbered
@@ -707,8 +707,8 @@ hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, ui
   const dim3 grid(per_xcd ? per_xcd * static_cast<uint32_t>(kXcds) : nblocks);
   uint32_t* counts = scratch;
   uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
-  for (int shift = 0; shift < bits; shift += kSortBits) {
-    if (shift > 0 || !first_counted)
+  for (int shift = shift0; shift < shift0 + bits; shift += kSortBits) {
+    if (shift > shift0 || !first_counted)
       hipLaunchKernelGGL(sort_hist_kernel, grid, dim3(kBlockThreads), 0, stream, keys, n, shift,
                          counts, nblocks, per_xcd, n_dev);
     hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,

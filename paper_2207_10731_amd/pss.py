@@ -29,6 +29,7 @@ PSS_BWD_MASK = 3
 PSS_SIGN_PM1, PSS_SIGN_SPARSE, PSS_SIGN_MASK = 1 << 2, 2 << 2, 3 << 2
 PSS_POOL_MEAN, PSS_INDEX_I32, PSS_ROWS_BF16 = 1 << 4, 1 << 5, 1 << 6
 PSS_PREPARE_BACKWARD = 1 << 7
+PSS_DEPOSIT_BY_ADDRESS = 1 << 8
 
 
 class PssError(RuntimeError):

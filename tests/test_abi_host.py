@@ -40,16 +40,16 @@ def test_measurement_library_is_separate(lib):
 
 
 def test_flag_layout(lib):
-    """Backward variant in bits 0-1, options in bits 2-7; the sign field value
-    3 << 2 and any bit from 8 up are rejected before anything is enqueued."""
+    """Backward variant in bits 0-1, options in bits 2-8; the sign field value
+    3 << 2 and any bit from 9 up are rejected before anything is enqueued."""
     assert pss.PSS_BWD_MASK == 3
     opts = [pss.PSS_SIGN_PM1, pss.PSS_SIGN_SPARSE, pss.PSS_POOL_MEAN, pss.PSS_INDEX_I32,
-            pss.PSS_ROWS_BF16, pss.PSS_PREPARE_BACKWARD]
+            pss.PSS_ROWS_BF16, pss.PSS_PREPARE_BACKWARD, pss.PSS_DEPOSIT_BY_ADDRESS]
     for f in opts:
-        assert f & 3 == 0 and f < (1 << 8)
+        assert f & 3 == 0 and f < (1 << 9)
     assert pss.PSS_SIGN_MASK == 3 << 2
     hp = pss.make_hash_params(1, num_tables=1, batch=1, num_indices=1)
-    for bad in [pss.PSS_SIGN_MASK, 1 << 8, 1 << 31]:
+    for bad in [pss.PSS_SIGN_MASK, 1 << 9, 1 << 31]:
         hp.flags = bad
         st = lib.pss_forward(ctypes.c_void_p(8), 4096, 4, 16, ctypes.byref(hp), ctypes.c_void_p(8),
                              ctypes.c_void_p(8), ctypes.c_void_p(8), None)
@@ -171,7 +171,7 @@ def _bad_call(lib, **kw):
 
 @pytest.mark.parametrize("kw", [dict(M=0), dict(M=2**31), dict(Z=0), dict(Z=5000, M=4096),
                                 dict(Z=3), dict(d=4097 * 4), dict(a=0), dict(a=P),
-                                dict(b=P), dict(T=0), dict(B=0), dict(N=-1), dict(flags=1 << 8),
+                                dict(b=P), dict(T=0), dict(B=0), dict(N=-1), dict(flags=1 << 9),
                                 dict(flags=3 << 2), dict(flags=pss.PSS_SIGN_PM1, sign_a=0),
                                 dict(flags=pss.PSS_SIGN_SPARSE, sign_a=P),
                                 dict(flags=pss.PSS_SIGN_PM1, sign_b=P),
@@ -196,7 +196,7 @@ def test_backward_rejects_bad_arguments(lib):
     hp_neg = pss.pss_hash_params(5, 7, 4, 2, 8, 0, -1.0, 0)
     assert f(dummy, dummy, 4096, 4, 16, ctypes.byref(hp_neg), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
-    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 1 << 8)
+    hp4 = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, 1 << 9)
     assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp4), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_ERR_INVALID_ARG
 

@@ -110,25 +110,28 @@ __global__ __launch_bounds__(kBlockThreads) void addr_records_kernel(
 // starts[x] = first record of tile x (records sorted by tile), for x in
 // [0, ntiles]; starts[ntiles] = n.  Position i writes the starts of the
 // tiles after the one of record i - 1 up to its own, so every entry is
-// written exactly once.
+// written exactly once.  A thread takes 4 consecutive positions.
 __global__ __launch_bounds__(kBlockThreads) void addr_starts_kernel(const uint32_t* __restrict__ keys,
                                                                     const uint32_t n, const uint32_t ntiles,
                                                                     uint32_t* __restrict__ starts) {
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlockThreads;
-  for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; i <= n;
-       i += stride) {
-    uint32_t tile = ntiles;
-    if (i < n) {
-      tile = keys[i] >> kAddrTileShift;
-      if (tile > ntiles - 1) tile = ntiles - 1;  // addresses are below M; guards memory anyway
+  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlockThreads * 4;
+  auto tile_of = [&](uint64_t i) -> int64_t {
+    if (i >= n) return ntiles;
+    const uint32_t t = keys[i] >> kAddrTileShift;
+    return t > ntiles - 1 ? ntiles - 1 : t;  // addresses are below M; guards memory anyway
+  };
+  for (uint64_t i0 = (static_cast<uint64_t>(blockIdx.x) * kBlockThreads + threadIdx.x) * 4; i0 <= n;
+       i0 += stride) {
+    int64_t t[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) t[j] = tile_of(i0 + j);
+    int64_t prev = i0 > 0 ? tile_of(i0 - 1) : -1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (i0 + j > n) break;
+      for (int64_t x = prev + 1; x <= t[j]; ++x) starts[x] = static_cast<uint32_t>(i0 + j);
+      prev = t[j];
     }
-    int64_t prev = -1;
-    if (i > 0) {
-      uint32_t tp = keys[i - 1] >> kAddrTileShift;
-      prev = tp > ntiles - 1 ? ntiles - 1 : tp;
-    }
-    for (int64_t x = prev + 1; x <= static_cast<int64_t>(tile); ++x)
-      starts[x] = static_cast<uint32_t>(i);
   }
 }
 
@@ -231,7 +234,7 @@ hipError_t launch_deposit_addr(float* dst, bool assign, float scale, const KPara
                          false, kAddrTileShift);
     if (e != hipSuccess) return e;
   }
-  const uint64_t want = (n + 1 + kBlockThreads - 1) / kBlockThreads;
+  const uint64_t want = (n + 1 + 4 * kBlockThreads - 1) / (4 * kBlockThreads);
   const uint32_t sgrid = static_cast<uint32_t>(want < 8192 ? want : 8192);
   hipLaunchKernelGGL(addr_starts_kernel, dim3(sgrid), dim3(kBlockThreads), 0, stream, k0,
                      static_cast<uint32_t>(n), ntiles, starts);

@@ -3,8 +3,10 @@ elements (8.6 GB).  Indices are chosen so that chunks start at elements
 M - 1, M - Z + 1 (both wrap to element 0), M - Z (ends exactly at M - 1) and
 0, next to the extreme index values 0 and 2^31 - 1 and random ones, in bags
 of zero to four items.  The forward is checked against the oracle on every
-bag, and each backward variant (SGD and Adagrad) on every element the batch
-reads, the elements around the wrap, and random untouched ones."""
+bag, and each backward variant (SGD and Adagrad; the deposit by address sorts
+on 17 tile bits here, three radix passes, and ends on a ragged tile) on every
+element the batch reads, the elements around the wrap, and random untouched
+ones."""
 import numpy as np
 import pytest
 import torch
@@ -89,8 +91,9 @@ def test_max_array_forward(batch):
 
 
 @pytest.mark.parametrize("opt", ["sgd", "adagrad"])
-@pytest.mark.parametrize("variant", [pss.PSS_BWD_ATOMIC, pss.PSS_BWD_SORTED, pss.PSS_BWD_SPARSE],
-                         ids=["atomic", "sorted", "sparse"])
+@pytest.mark.parametrize("variant", [pss.PSS_BWD_ATOMIC, pss.PSS_BWD_SORTED, pss.PSS_BWD_SPARSE,
+                                     pss.PSS_BWD_SORTED | pss.PSS_DEPOSIT_BY_ADDRESS],
+                         ids=["atomic", "sorted", "sparse", "by-address"])
 def test_max_array_backward(batch, variant, opt):
     dev, shared, idx, off, hp = _setup(batch, variant)
     state = torch.zeros(M, device=dev) if opt == "adagrad" else None

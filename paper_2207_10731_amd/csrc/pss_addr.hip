@@ -13,7 +13,8 @@
 //            a chunk of factor 0 gives -0.0, which changes nothing
 //   sort     LSD radix sort of the records by address tile (the address bits
 //            from kAddrTileShift up; 8-bit digits, stable)
-//   starts   first record of every tile, from the sorted addresses
+//   starts   first record of every tile: a binary search of the sorted
+//            addresses per tile
 //   apply    one workgroup per tile of 2^kAddrTileShift elements: the tile's
 //            records are summed into an LDS copy of the tile (LDS float
 //            atomics, initialised to -0.0 so that an element without records
@@ -108,31 +109,21 @@ __global__ __launch_bounds__(kBlockThreads) void addr_records_kernel(
 }
 
 // starts[x] = first record of tile x (records sorted by tile), for x in
-// [0, ntiles]; starts[ntiles] = n.  Position i writes the starts of the
-// tiles after the one of record i - 1 up to its own, so every entry is
-// written exactly once.  A thread takes 4 consecutive positions.
+// [0, ntiles]; starts[ntiles] = n.  One thread per entry: a binary search
+// for the first record whose tile is at least x.
 __global__ __launch_bounds__(kBlockThreads) void addr_starts_kernel(const uint32_t* __restrict__ keys,
                                                                     const uint32_t n, const uint32_t ntiles,
                                                                     uint32_t* __restrict__ starts) {
-  const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlockThreads * 4;
-  auto tile_of = [&](uint64_t i) -> int64_t {
-    if (i >= n) return ntiles;
-    const uint32_t t = keys[i] >> kAddrTileShift;
-    return t > ntiles - 1 ? ntiles - 1 : t;  // addresses are below M; guards memory anyway
-  };
-  for (uint64_t i0 = (static_cast<uint64_t>(blockIdx.x) * kBlockThreads + threadIdx.x) * 4; i0 <= n;
-       i0 += stride) {
-    int64_t t[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) t[j] = tile_of(i0 + j);
-    int64_t prev = i0 > 0 ? tile_of(i0 - 1) : -1;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (i0 + j > n) break;
-      for (int64_t x = prev + 1; x <= t[j]; ++x) starts[x] = static_cast<uint32_t>(i0 + j);
-      prev = t[j];
-    }
+  const uint32_t x = blockIdx.x * kBlockThreads + threadIdx.x;
+  if (x > ntiles) return;
+  uint32_t lo = 0, hi = n;
+  while (lo < hi) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    uint32_t t = keys[mid] >> kAddrTileShift;
+    t = t > ntiles - 1 ? ntiles - 1 : t;  // addresses are below M; guards memory anyway
+    if (t < x) lo = mid + 1; else hi = mid;
   }
+  starts[x] = lo;
 }
 
 // One workgroup per tile of the array: sum the tile's records in LDS, then
@@ -234,8 +225,7 @@ hipError_t launch_deposit_addr(float* dst, bool assign, float scale, const KPara
                          false, kAddrTileShift);
     if (e != hipSuccess) return e;
   }
-  const uint64_t want = (n + 1 + 4 * kBlockThreads - 1) / (4 * kBlockThreads);
-  const uint32_t sgrid = static_cast<uint32_t>(want < 8192 ? want : 8192);
+  const uint32_t sgrid = (ntiles + 1 + kBlockThreads - 1) / kBlockThreads;
   hipLaunchKernelGGL(addr_starts_kernel, dim3(sgrid), dim3(kBlockThreads), 0, stream, k0,
                      static_cast<uint32_t>(n), ntiles, starts);
   hipLaunchKernelGGL(addr_apply_kernel, dim3(ntiles), dim3(kApplyThreads), 0, stream, dst,

@@ -11,9 +11,11 @@
 //             the pooled row its gradient is read from.
 //   sort      LSD radix sort of the (h0, r) pairs on the low 8, 16 or 24
 //             bits of h0 (groups of at most ~8192 pairs), 8-bit digits, stable;
-//             per pass a histogram kernel, a per-digit scan (one workgroup
-//             per digit) and a scatter kernel whose per-wave ranks come from
-//             ballot matching (no atomics on the data path).
+//             per pass a histogram kernel (two tiles per workgroup), a scan
+//             of the per-tile digit counts (one workgroup per digit, or per
+//             digit and chunk of 4096 tiles for long inputs) and a scatter
+//             kernel whose per-wave ranks come from ballot matching (no
+//             atomics on the data path).
 //   reduce    one workgroup per 256 consecutive sorted pairs: sort them by
 //             the full h0 (bitonic network per wavefront, then a merge of
 //             the four lists through LDS), accumulate the gradient rows of
@@ -119,35 +121,50 @@ __device__ __forceinline__ int64_t live_count(int64_t n, const uint32_t* n_dev) 
 }
 
 // counts[d * nblocks + tile] = number of keys of the tile with digit d.
+// A workgroup counts kHistTiles consecutive tiles (two wavefronts per
+// tile, 16 keys per lane, all requested before any is counted), so that
+// more of the keys are in flight at once.  `pair` numbering follows
+// sort_tile_index over the groups of tiles.
+constexpr int kHistTiles = 2;
+constexpr int kHistKeysPerLane = kSortTile * kHistTiles / kBlockThreads;
+constexpr int kHistWaveKeys = kHistKeysPerLane * kWave;
+static_assert(kWavesPerBlock == 2 * kHistTiles, "two wavefronts per tile");
 __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
     const uint32_t* __restrict__ keys, int64_t n, const int shift,
     uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t per_xcd,
     const uint32_t* __restrict__ n_dev) {
-  const uint32_t tile = sort_tile_index(per_xcd);
-  if (tile >= nblocks) return;
+  const uint32_t group = sort_tile_index(per_xcd);
+  const uint32_t tile0 = group * kHistTiles;
+  if (tile0 >= nblocks) return;
   n = live_count(n, n_dev);
-  // no live key in this tile: the scan reads the live tiles' counts only
-  if (static_cast<int64_t>(tile) * kSortTile >= n) return;
+  // no live key in these tiles: the scan reads the live tiles' counts only
+  if (static_cast<int64_t>(tile0) * kSortTile >= n) return;
   __shared__ uint32_t hist[kWavesPerBlock][kBins];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
-  __syncthreads();
-  const int64_t base = static_cast<int64_t>(tile) * kSortTile + w * kWaveSortKeys;
-#pragma unroll 4
-  for (int s = 0; s < kSortItemsPerLane; ++s) {
+  const int64_t base = static_cast<int64_t>(tile0) * kSortTile + w * kHistWaveKeys;
+  uint32_t kx[kHistKeysPerLane];
+#pragma unroll
+  for (int s = 0; s < kHistKeysPerLane; ++s) {
     const int64_t idx = base + s * kWave + lane;
-    const bool valid = idx < n;
-    const uint32_t digit = valid ? (keys[idx] >> shift) & (kBins - 1) : 0u;
+    kx[s] = idx < n ? keys[idx] : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < kHistKeysPerLane; ++s) {
+    const bool valid = base + s * kWave + lane < n;
+    const uint32_t digit = (kx[s] >> shift) & (kBins - 1);
     const uint64_t eq = match_digit(digit, valid);
     // the lowest lane of each group adds the group's size (wave-private row)
     if (valid && (eq & lanes_below(lane)) == 0) hist[w][digit] += __popcll(eq);
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
-    uint32_t s = 0;
+  const int d = threadIdx.x;  // one digit per thread
 #pragma unroll
-    for (int ww = 0; ww < kWavesPerBlock; ++ww) s += hist[ww][d];
-    counts[static_cast<uint64_t>(d) * nblocks + tile] = s;
+  for (int t = 0; t < kHistTiles; ++t) {
+    const uint32_t tile = tile0 + t;
+    if (tile < nblocks && static_cast<int64_t>(tile) * kSortTile < n)
+      counts[static_cast<uint64_t>(d) * nblocks + tile] = hist[2 * t][d] + hist[2 * t + 1][d];
   }
 }
 
@@ -250,44 +267,116 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
   }
 }
 
+// Scans of the count rows.  A chunk of kScanChunk consecutive entries is
+// scanned by the workgroup's wavefronts, each a contiguous quarter read and
+// written 64 entries (one line) per instruction.
+constexpr int kScanPerThread = 16;
+constexpr uint32_t kScanChunk = kBlockThreads * kScanPerThread;
+constexpr uint32_t kScanWaveEntries = kScanChunk / kWavesPerBlock;
+
+// Exclusive scan in place of row[c0, min(c0 + kScanChunk, end)), every
+// entry raised by `carry`; returns the chunk's sum.
+__device__ __forceinline__ uint32_t scan_chunk(uint32_t* __restrict__ row, const uint32_t c0,
+                                               const uint32_t end, const uint32_t carry,
+                                               uint32_t* wsum) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  const uint32_t q0 = c0 + w * kScanWaveEntries;
+  uint32_t v[kScanPerThread];
+#pragma unroll
+  for (int j = 0; j < kScanPerThread; ++j) {
+    const uint32_t i = q0 + j * kWave + lane;
+    v[j] = i < end ? row[i] : 0u;
+  }
+  uint32_t run = 0;  // sum of the wavefront's earlier groups of 64
+#pragma unroll
+  for (int j = 0; j < kScanPerThread; ++j) {
+    uint32_t x = v[j];
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const uint32_t y = __shfl_up(x, off);
+      if (lane >= off) x += y;
+    }
+    const uint32_t excl = run + x - v[j];
+    run += __shfl(x, kWave - 1);
+    v[j] = excl;
+  }
+  if (lane == 0) wsum[w] = run;
+  __syncthreads();
+  uint32_t before = carry, all = 0;
+#pragma unroll
+  for (int ww = 0; ww < kWavesPerBlock; ++ww) {
+    before += ww < w ? wsum[ww] : 0u;
+    all += wsum[ww];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kScanPerThread; ++j) {
+    const uint32_t i = q0 + j * kWave + lane;
+    if (i < end) row[i] = before + v[j];
+  }
+  return all;
+}
+
+__device__ __forceinline__ uint32_t live_tiles(int64_t n, const uint32_t* n_dev, uint32_t nblocks) {
+  n = live_count(n, n_dev);
+  const uint64_t live = (static_cast<uint64_t>(n) + kSortTile - 1) / kSortTile;
+  return live < nblocks ? static_cast<uint32_t>(live) : nblocks;
+}
+
 // Row d of counts (one digit, one entry per tile): exclusive scan in place
 // over the tiles that hold live keys (the others are never read: their
 // scatter workgroups exit at once); totals[d] = the row's sum.  One
-// workgroup per digit.
-constexpr int kScanPerThread = 16;
+// workgroup per digit, for rows of a few chunks.
 __global__ __launch_bounds__(kBlockThreads) void sort_scan_kernel(uint32_t* __restrict__ counts,
                                                                   const uint32_t nblocks,
                                                                   uint32_t* __restrict__ totals,
                                                                   int64_t n,
                                                                   const uint32_t* __restrict__ n_dev) {
   __shared__ uint32_t wsum[kWavesPerBlock];
-  n = live_count(n, n_dev);
-  const uint64_t live = (static_cast<uint64_t>(n) + kSortTile - 1) / kSortTile;
-  const uint32_t ntiles = live < nblocks ? static_cast<uint32_t>(live) : nblocks;
+  const uint32_t ntiles = live_tiles(n, n_dev, nblocks);
   uint32_t* row = counts + static_cast<uint64_t>(blockIdx.x) * nblocks;
-  // entries per thread for this row (at most kScanPerThread per round)
-  const uint32_t per = (ntiles + kBlockThreads - 1) / kBlockThreads;
-  const uint32_t pt = per < 1 ? 1 : (per < kScanPerThread ? per : kScanPerThread);
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < ntiles; base += pt * kBlockThreads) {
-    const uint32_t i0 = base + threadIdx.x * pt;
-    uint32_t v[kScanPerThread];
-    uint32_t sum = 0;
-#pragma unroll
-    for (int j = 0; j < kScanPerThread; ++j) {
-      v[j] = (static_cast<uint32_t>(j) < pt && i0 + j < ntiles) ? row[i0 + j] : 0u;
-      sum += v[j];
-    }
-    uint32_t tot;
-    uint32_t run = carry + block_exclusive_scan(sum, wsum, &tot);
-#pragma unroll
-    for (int j = 0; j < kScanPerThread; ++j) {
-      if (static_cast<uint32_t>(j) < pt && i0 + j < ntiles) row[i0 + j] = run;
-      run += v[j];
-    }
-    carry += tot;
-  }
+  for (uint32_t c0 = 0; c0 < ntiles; c0 += kScanChunk) carry += scan_chunk(row, c0, ntiles, carry, wsum);
   if (threadIdx.x == 0) totals[blockIdx.x] = carry;
+}
+
+// Longer rows: grid (chunk, digit).  sort_scan_sums_kernel writes each
+// chunk's sum into partial[digit * nchunks + chunk]; sort_scan_apply_kernel
+// scans the chunk after the sums of the row's earlier chunks, and the last
+// live chunk writes totals[digit].
+__global__ __launch_bounds__(kBlockThreads) void sort_scan_sums_kernel(
+    const uint32_t* __restrict__ counts, const uint32_t nblocks, uint32_t* __restrict__ partial,
+    int64_t n, const uint32_t* __restrict__ n_dev) {
+  __shared__ uint32_t wsum[kWavesPerBlock];
+  const uint32_t ntiles = live_tiles(n, n_dev, nblocks);
+  const uint32_t c0 = blockIdx.x * kScanChunk;
+  if (c0 >= ntiles) return;
+  const uint32_t* row = counts + static_cast<uint64_t>(blockIdx.y) * nblocks;
+  uint32_t sum = 0;
+#pragma unroll
+  for (int j = 0; j < kScanPerThread; ++j) {
+    const uint32_t i = c0 + j * kBlockThreads + threadIdx.x;
+    sum += i < ntiles ? row[i] : 0u;
+  }
+  uint32_t tot;
+  block_exclusive_scan(sum, wsum, &tot);
+  if (threadIdx.x == 0) partial[static_cast<uint64_t>(blockIdx.y) * gridDim.x + blockIdx.x] = tot;
+}
+__global__ __launch_bounds__(kBlockThreads) void sort_scan_apply_kernel(
+    uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t* __restrict__ partial,
+    uint32_t* __restrict__ totals, int64_t n, const uint32_t* __restrict__ n_dev) {
+  __shared__ uint32_t wsum[kWavesPerBlock];
+  const uint32_t ntiles = live_tiles(n, n_dev, nblocks);
+  const uint32_t c0 = blockIdx.x * kScanChunk;
+  if (c0 >= ntiles) return;
+  const uint32_t* prow = partial + static_cast<uint64_t>(blockIdx.y) * gridDim.x;
+  uint32_t pre = 0;  // sum of the row's earlier chunks (each thread a strided share)
+  for (uint32_t c = threadIdx.x; c < blockIdx.x; c += kBlockThreads) pre += prow[c];
+  uint32_t carry;
+  block_exclusive_scan(pre, wsum, &carry);
+  uint32_t* row = counts + static_cast<uint64_t>(blockIdx.y) * nblocks;
+  const uint32_t tot = scan_chunk(row, c0, ntiles, carry, wsum);
+  if (threadIdx.x == 0 && c0 + kScanChunk >= ntiles) totals[blockIdx.y] = carry + tot;
 }
 
 // Stable scatter of one tile by digit into its global slots.  The tile is
@@ -685,9 +774,11 @@ static uint32_t sort_tiles_per_xcd(uint32_t nblocks) {
   return static_cast<uint32_t>((nblocks + kXcds - 1) / kXcds);
 }
 
+static uint32_t scan_chunks(uint32_t nblocks) { return (nblocks + kScanChunk - 1) / kScanChunk; }
+
 size_t radix_scratch_bytes(int64_t n) {
   const uint64_t nblocks = (static_cast<uint64_t>(n) + kSortTile - 1) / kSortTile;
-  return (nblocks * kBins + kBins) * 4 + 256;
+  return (nblocks * kBins + kBins + static_cast<uint64_t>(kBins) * scan_chunks(static_cast<uint32_t>(nblocks))) * 4 + 256;
 }
 
 size_t sorted_workspace_bytes(const KParams& p) {
@@ -705,14 +796,26 @@ hipError_t radix_sort_pairs(uint32_t*& keys, uint32_t*& vals, uint32_t* ktmp, ui
   // in dispatch order so that they spread over every XCD
   const uint32_t per_xcd = n_dev == nullptr ? sort_tiles_per_xcd(nblocks) : 0u;
   const dim3 grid(per_xcd ? per_xcd * static_cast<uint32_t>(kXcds) : nblocks);
+  const uint32_t ngroups = (nblocks + kHistTiles - 1) / kHistTiles;
+  const uint32_t hper_xcd = n_dev == nullptr ? sort_tiles_per_xcd(ngroups) : 0u;
+  const dim3 hgrid(hper_xcd ? hper_xcd * static_cast<uint32_t>(kXcds) : ngroups);
   uint32_t* counts = scratch;
   uint32_t* totals = counts + static_cast<uint64_t>(nblocks) * kBins;
   for (int shift = shift0; shift < shift0 + bits; shift += kSortBits) {
     if (shift > shift0 || !first_counted)
-      hipLaunchKernelGGL(sort_hist_kernel, grid, dim3(kBlockThreads), 0, stream, keys, n, shift,
-                         counts, nblocks, per_xcd, n_dev);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
-                       nblocks, totals, n, n_dev);
+      hipLaunchKernelGGL(sort_hist_kernel, hgrid, dim3(kBlockThreads), 0, stream, keys, n, shift,
+                         counts, nblocks, hper_xcd, n_dev);
+    const uint32_t nch = scan_chunks(nblocks);
+    if (nch <= 2) {
+      hipLaunchKernelGGL(sort_scan_kernel, dim3(kBins), dim3(kBlockThreads), 0, stream, counts,
+                         nblocks, totals, n, n_dev);
+    } else {
+      uint32_t* partial = totals + kBins;
+      hipLaunchKernelGGL(sort_scan_sums_kernel, dim3(nch, kBins), dim3(kBlockThreads), 0, stream,
+                         counts, nblocks, partial, n, n_dev);
+      hipLaunchKernelGGL(sort_scan_apply_kernel, dim3(nch, kBins), dim3(kBlockThreads), 0, stream,
+                         counts, nblocks, partial, totals, n, n_dev);
+    }
     hipLaunchKernelGGL(sort_scatter_kernel, grid, dim3(kBlockThreads), 0, stream, keys, vals,
                        ktmp, vtmp, n, shift, counts, nblocks, totals, per_xcd, n_dev);
     const hipError_t e = hipGetLastError();

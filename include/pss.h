@@ -43,25 +43,38 @@
  *   PSS_INDEX_I32  indices and offsets are int32.
  *   PSS_ROWS_BF16  out is written, and grad_out read, as bfloat16 (out is
  *     rounded to nearest even from the float32 result).
- *   PSS_DEPOSIT_BY_ADDRESS  with the SORTED variant (or AUTO): every (lookup,
- *     dim) contribution becomes an (address, value) record, the records are
- *     radix-sorted by address tile (2^14 elements) and each tile's records
- *     are summed on chip and applied to the array (or the float32 gradient
- *     buffer) in one pass: no float atomics to memory, at the cost of 16 B
- *     of scratch per (lookup, dim).  Requires N * d < 2^31 (else
- *     PSS_ERR_UNSUPPORTED); invalid with ATOMIC or SPARSE
- *     (PSS_ERR_UNSUPPORTED).  AUTO takes it by itself for chunks shorter than
- *     a 64-byte memory line (Z < 16) on an array beyond the memory-side cache
- *     (M * 4 > 256 MiB), where lookups seldom repeat and each contribution
- *     would otherwise be an atomic to its own line.
+ *   PSS_DEPOSIT_BY_ADDRESS  with the SORTED variant (or AUTO): the deposit
+ *     is ordered by address instead of made with float atomics to memory.
+ *     The contributions are radix-sorted by address tile (2^14 elements)
+ *     and each tile sums its contributions on chip and is updated once.
+ *     - Z < 64: every (lookup, dim) contribution is its own (address, value)
+ *       record; the tile is applied to the array (SGD on float32) or stored
+ *       as that tile of the float32 gradient buffer before the optimizer
+ *       pass.  16 B of scratch per (lookup, dim).  AUTO takes this by itself
+ *       for chunks shorter than a 64-byte memory line (Z < 16) on an array
+ *       beyond the memory-side cache (M * 4 > 256 MiB), where lookups seldom
+ *       repeat and each contribution would otherwise be an atomic to its
+ *       own line.
+ *     - Z >= 64: the lookups are grouped by token first (as SORTED does) and
+ *       each run sum becomes one record per chunk (Z values); each tile adds
+ *       the chunks reaching it in a fixed order and applies the optimizer to
+ *       its elements in place (no gradient buffer, no dense pass).  Every
+ *       sum is taken in a fixed order, so the update is bit-identical run to
+ *       run.  Scratch: N * d floats of run sums plus 20 B per (lookup,
+ *       chunk).  AUTO never takes this one (the atomic deposit of whole-line
+ *       chunks is as fast); it uses a grouping made ahead by
+ *       PSS_PREPARE_BACKWARD like SORTED.  Requires N * (d/Z) < 2^31.
+ *     Both require N * d < 2^31 (else PSS_ERR_UNSUPPORTED); the flag is
+ *     invalid with ATOMIC or SPARSE (PSS_ERR_UNSUPPORTED).
  *   PSS_PREPARE_BACKWARD  read by pss_forward only (the other calls ignore
  *     it; pss_prepare_backward does the same work as a call of its own): the
  *     forward also groups the batch's lookups by token for the backward, on
  *     a library-owned stream that runs beside the forward kernel.  The next
  *     pss_backward_update on the same stream uses that grouping when its
  *     indices and offsets pointers, batch shape, hash parameters and options
- *     match and it runs the SORTED variant (AUTO's choice for SGD on float32
- *     storage); it drops the grouping either way.  The match is by pointer:
+ *     match and it runs the SORTED variant grouped by token (AUTO's choice
+ *     for SGD on float32 storage; also the run sums by address of
+ *     PSS_DEPOSIT_BY_ADDRESS with Z >= 64); it drops the grouping either way.  The match is by pointer:
  *     the library records the indices and offsets pointers of the prepared
  *     batch (comparing them later, never reading through them after the
  *     grouping's own work) and cannot see their contents, so the caller must
@@ -74,7 +87,8 @@
  *     by a new preparation on the same stream), `stream` first waits for it:
  *     work the caller enqueues there afterwards follows its reads of the old
  *     indices and offsets.  Ignored while the stream is being captured into a
- *     graph, and for an explicit ATOMIC or SPARSE variant; if the grouping
+ *     graph, for an explicit ATOMIC or SPARSE variant and for a deposit by
+ *     address of single contributions (Z < 64); if the grouping
  *     cannot be set up (no memory for its buffer), the forward runs without
  *     it.  Holds one buffer of 16 B per lookup per stream (see "Memory").
  * Shared array.  `shared` holds M elements of the storage type named by
@@ -153,8 +167,9 @@ enum {
  *           pss_gradient_sparse, then the optimizer applied at those
  *           locations only.  No float atomics: bit-identical run to run.
  *           Requires N * (d/Z) < 2^31.
- * ATOMIC and SORTED sum in no fixed order; all variants compute the same G up
- * to float rounding. */
+ * ATOMIC and SORTED sum in no fixed order (SORTED with PSS_DEPOSIT_BY_ADDRESS
+ * and Z >= 64 in a fixed one); all variants compute the same G up to float
+ * rounding. */
 enum { PSS_BWD_AUTO = 0, PSS_BWD_ATOMIC = 1, PSS_BWD_SORTED = 2, PSS_BWD_SPARSE = 3 };
 #define PSS_BWD_MASK 3u
 

@@ -21,6 +21,16 @@
 //            keeps its bits), then the tile is added to dst in one streaming
 //            pass (fused SGD) or stored as the tile of a float32 gradient
 //            buffer (every element of it, so the buffer needs no zero-fill).
+//
+// Run sums by address (chunks of 64 elements or more, updates through G):
+// the lookups are first grouped by token as for the grouped deposit, and
+// each run's summed gradient row becomes the contribution: one record per
+// run and chunk, (chunk base, payload row of Z values).  The records are
+// radix-sorted by the tile of their base, and one workgroup per tile sums
+// the payloads of every chunk that reaches the tile (its own, the previous
+// tile's spilling over the boundary and, for tile 0, those wrapping past M)
+// in LDS, then applies SGD or Adagrad to the tile's elements in place: no
+// float atomics to memory, no G buffer, no dense optimizer pass.
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -109,7 +119,7 @@ __global__ __launch_bounds__(kBlockThreads) void addr_records_kernel(
 }
 
 // starts[x] = first record of tile x (records sorted by tile), for x in
-// [0, ntiles]; starts[ntiles] = n.  One thread per entry: a binary search
+// [0, ntiles]; starts[ntiles] = the number of records with an address.  One thread per entry: a binary search
 // for the first record whose tile is at least x.
 __global__ __launch_bounds__(kBlockThreads) void addr_starts_kernel(const uint32_t* __restrict__ keys,
                                                                     const uint32_t n, const uint32_t ntiles,
@@ -120,7 +130,7 @@ __global__ __launch_bounds__(kBlockThreads) void addr_starts_kernel(const uint32
   while (lo < hi) {
     const uint32_t mid = lo + ((hi - lo) >> 1);
     uint32_t t = keys[mid] >> kAddrTileShift;
-    t = t > ntiles - 1 ? ntiles - 1 : t;  // addresses are below M; guards memory anyway
+    t = t > ntiles ? ntiles : t;  // records without an address (kNoRecord) sort last
     if (t < x) lo = mid + 1; else hi = mid;
   }
   starts[x] = lo;
@@ -230,6 +240,214 @@ hipError_t launch_deposit_addr(float* dst, bool assign, float scale, const KPara
                      static_cast<uint32_t>(n), ntiles, starts);
   hipLaunchKernelGGL(addr_apply_kernel, dim3(ntiles), dim3(kApplyThreads), 0, stream, dst,
                      assign ? 1u : 0u, p.M, k0, v0, starts);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Run sums by address
+// ---------------------------------------------------------------------------
+constexpr int kRunsApplyThreads = 1024;
+constexpr int kRunsBatch = 8;  // records whose payload pieces are requested together
+constexpr int kRunsOpt = 4;    // elements per lane updated together
+constexpr uint32_t kRunsStage = 1024;  // records staged in LDS at a time
+
+// Whether the chunk of Z elements from `base` (wrapping past M) has an
+// element in [x0, x0 + len).
+__device__ __forceinline__ bool chunk_reaches(uint32_t base, uint32_t Z, uint32_t M, uint32_t x0,
+                                              uint32_t len) {
+  const uint64_t last = static_cast<uint64_t>(base) + Z - 1;
+  if (last < M) return base < x0 + len && last >= x0;
+  return base < x0 + len || x0 <= last - M;  // [base, M) and [0, last - M]
+}
+
+// One workgroup per tile of the array, each of its wavefronts owning a
+// range of kRunsRange consecutive elements of the tile in LDS.  Records are
+// (base, slot): the chunk covers elements (base + k) mod M, k < Z, with
+// values payload[slot * Z + k].  Every wavefront walks the records of the
+// tiles whose chunks can reach this one and adds the part of each chunk
+// that falls in its own range with plain LDS read-add-writes: no two
+// wavefronts touch one element, and a wavefront adds one chunk at a time
+// (its lanes on distinct elements), so no atomics are needed and each
+// element's sum is taken in the records' sorted order.  The wavefront then
+// applies the update to its range.
+constexpr uint32_t kRunsRange = kAddrTile / (kRunsApplyThreads / kWave);  // 1024
+
+template <typename WT, bool ADAGRAD>
+__global__ __launch_bounds__(kRunsApplyThreads) void runs_apply_kernel(
+    WT* __restrict__ w, float* __restrict__ s, const uint32_t M, const uint32_t Z,
+    const uint32_t ntiles, const uint32_t* __restrict__ keys, const uint32_t* __restrict__ slots,
+    const uint32_t* __restrict__ starts, const float* __restrict__ payload, const float lr,
+    const float eps) {
+  __shared__ float tile[kAddrTile];
+  const uint32_t x = blockIdx.x;
+  const uint32_t x0 = x << kAddrTileShift;
+  const uint32_t len = M - x0 < kAddrTile ? M - x0 : kAddrTile;
+  // Tiles whose chunks can reach this one: itself; the previous tile (a
+  // chunk of at most 4096 elements crosses at most one boundary of a full
+  // tile); for tile 0 the last two (chunks wrapping past M, the last tile
+  // possibly shorter than a chunk).
+  uint32_t src[3];
+  int nsrc = 0;
+  src[nsrc++] = x;
+  if (x >= 1) src[nsrc++] = x - 1;
+  if (x == 0 && ntiles >= 2) src[nsrc++] = ntiles - 1;
+  if (x == 0 && ntiles >= 3) src[nsrc++] = ntiles - 2;
+  uint32_t total = 0;
+  for (int i = 0; i < nsrc; ++i) total += starts[src[i] + 1] - starts[src[i]];
+  if (total == 0) return;  // whole workgroup: G = 0 on this tile, nothing changes
+  __shared__ uint32_t sbase[kRunsStage], sslot[kRunsStage];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  // this wavefront's elements: [r0, r0 + rlen) of the array
+  const uint32_t r0 = x0 + wv * kRunsRange;
+  const uint32_t rend = x0 + len;
+  const uint32_t rlen = r0 >= rend ? 0u : (rend - r0 < kRunsRange ? rend - r0 : kRunsRange);
+  float* acc = tile + wv * kRunsRange;
+  for (uint32_t i = lane; i < kRunsRange; i += kWave) acc[i] = 0.f;
+  bool touched = false;
+  for (int i = 0; i < nsrc; ++i) {
+    const uint32_t lo = starts[src[i]], hi = starts[src[i] + 1];
+    for (uint32_t c0 = lo; c0 < hi; c0 += kRunsStage) {
+      // the workgroup stages up to kRunsStage records in LDS; every
+      // wavefront then picks those reaching its range
+      const uint32_t cn = hi - c0 < kRunsStage ? hi - c0 : kRunsStage;
+      __syncthreads();  // the previous stage has been read
+      for (uint32_t j = threadIdx.x; j < cn; j += kRunsApplyThreads) {
+        sbase[j] = keys[c0 + j];
+        sslot[j] = slots[c0 + j];
+      }
+      __syncthreads();
+      if (rlen == 0) continue;  // past the end of a short last tile
+      for (uint32_t b0 = 0; b0 < cn; b0 += kWave) {
+        uint32_t base = 0, slot = 0;
+        bool reach = false;
+        if (b0 + lane < cn) {
+          base = sbase[b0 + lane];
+          slot = sslot[b0 + lane];
+          reach = chunk_reaches(base, Z, M, r0, rlen);
+        }
+        uint64_t todo = __ballot(reach);
+        touched |= todo != 0;
+        while (todo) {
+          // up to kRunsBatch records: their payload pieces are requested
+          // before any is added
+          uint32_t qs[kRunsBatch];
+          int nq = 0;
+#pragma unroll
+          for (int u = 0; u < kRunsBatch; ++u) {
+            qs[u] = todo ? static_cast<uint32_t>(__builtin_ctzll(todo)) : qs[0];
+            if (todo) {
+              todo &= todo - 1;
+              ++nq;
+            }
+          }
+          for (uint32_t k0 = 0; k0 < Z; k0 += kWave) {
+            const uint32_t k = k0 + lane;
+            float v[kRunsBatch];
+            uint32_t off[kRunsBatch];
+#pragma unroll
+            for (int u = 0; u < kRunsBatch; ++u) {
+              const uint32_t bq = readlane_u32(base, qs[u]);
+              uint32_t m = bq + k;  // bq < M and k < Z <= M: no overflow
+              if (m >= M) m -= M;
+              off[u] = m - r0;  // below rlen exactly when m is in the range
+              v[u] = 0.f;
+              if (u < nq && k < Z && off[u] < rlen)
+                v[u] = payload[static_cast<uint64_t>(readlane_u32(slot, qs[u])) * Z + k];
+            }
+#pragma unroll
+            for (int u = 0; u < kRunsBatch; ++u)
+              if (u < nq && k < Z && off[u] < rlen) acc[off[u]] += v[u];
+          }
+        }
+      }
+    }
+  }
+  if (rlen == 0) return;
+  if (!touched) return;  // no chunk reaches this range: G = 0 on it
+  // Each element was written by this wavefront only (its own LDS writes are
+  // visible to it in program order).  The range's weights (and states) are
+  // read whole, kRunsOpt elements per lane at a time, then updated where
+  // G != 0 (elements with G == 0, and lanes past the range's end, store
+  // nothing).
+  for (uint32_t i0 = 0; i0 < rlen; i0 += kRunsOpt * kWave) {
+    float g[kRunsOpt];
+#pragma unroll
+    for (int u = 0; u < kRunsOpt; ++u) {
+      const uint32_t i = i0 + u * kWave + lane;
+      g[u] = i < rlen ? acc[i] : 0.f;
+    }
+    float wo[kRunsOpt], so[kRunsOpt];
+#pragma unroll
+    for (int u = 0; u < kRunsOpt; ++u) {
+      const uint32_t i = i0 + u * kWave + lane;
+      const int64_t m = static_cast<int64_t>(r0) + (i < rlen ? i : 0u);
+      wo[u] = load_weight64(w, m);
+      so[u] = ADAGRAD ? s[m] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kRunsOpt; ++u)
+      if (g[u] != 0.f)
+        update_loaded<WT, ADAGRAD>(w, s, static_cast<int64_t>(r0) + i0 + u * kWave + lane, g[u],
+                                   wo[u], so[u], lr, eps);
+  }
+}
+
+static int runs_sort_bits(uint32_t ntiles) {
+  int bits = 0;  // 2^bits > ntiles: kNoRecord's tile field lies past every tile
+  while ((1u << bits) <= ntiles) ++bits;
+  return bits;
+}
+
+size_t runs_workspace_bytes(const KParams& p) {
+  const uint64_t n = static_cast<uint64_t>(p.N) * p.C;
+  const uint64_t payload = (static_cast<uint64_t>(p.N) * p.d * 4 + 255) & ~uint64_t(255);
+  return payload + n * 16 + radix_scratch_bytes(static_cast<int64_t>(n)) +
+         (static_cast<size_t>(addr_tiles(p)) + 1) * 4 + 256;
+}
+
+hipError_t launch_deposit_runs(void* w, bool bf16, float* state, float lr, float eps,
+                               const KParams& p, const GroupedPairs& g, const void* grad,
+                               void* workspace, hipStream_t stream) {
+  const uint64_t n = static_cast<uint64_t>(p.N) * p.C;
+  if (n >= (1ull << 31) || p.Z > 4096) return hipErrorInvalidValue;
+  const uint32_t ntiles = addr_tiles(p);
+  float* payload = static_cast<float*>(workspace);
+  uint32_t* k0 = reinterpret_cast<uint32_t*>(
+      static_cast<char*>(workspace) +
+      ((static_cast<uint64_t>(p.N) * p.d * 4 + 255) & ~uint64_t(255)));
+  uint32_t* v0 = k0 + n;
+  uint32_t* k1 = v0 + n;
+  uint32_t* v1 = k1 + n;
+  uint32_t* scratch = v1 + n;
+  uint32_t* starts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(scratch) +
+                                                 radix_scratch_bytes(static_cast<int64_t>(n)));
+  if (n == 0) return hipSuccess;
+  hipError_t e = launch_reduce_records(payload, 1.f, p, g, grad, k0, v0, stream);
+  if (e != hipSuccess) return e;
+  e = radix_sort_pairs(k0, v0, k1, v1, static_cast<int64_t>(n), runs_sort_bits(ntiles), scratch,
+                       stream, nullptr, false, kAddrTileShift);
+  if (e != hipSuccess) return e;
+  const uint32_t sgrid = (ntiles + 1 + kBlockThreads - 1) / kBlockThreads;
+  hipLaunchKernelGGL(addr_starts_kernel, dim3(sgrid), dim3(kBlockThreads), 0, stream, k0,
+                     static_cast<uint32_t>(n), ntiles, starts);
+  const dim3 grid(ntiles), block(kRunsApplyThreads);
+  if (bf16) {
+    uint16_t* wb = static_cast<uint16_t*>(w);
+    if (state)
+      hipLaunchKernelGGL((runs_apply_kernel<uint16_t, true>), grid, block, 0, stream, wb, state,
+                         p.M, p.Z, ntiles, k0, v0, starts, payload, lr, eps);
+    else
+      hipLaunchKernelGGL((runs_apply_kernel<uint16_t, false>), grid, block, 0, stream, wb, state,
+                         p.M, p.Z, ntiles, k0, v0, starts, payload, lr, eps);
+  } else {
+    float* wf = static_cast<float*>(w);
+    if (state)
+      hipLaunchKernelGGL((runs_apply_kernel<float, true>), grid, block, 0, stream, wf, state, p.M,
+                         p.Z, ntiles, k0, v0, starts, payload, lr, eps);
+    else
+      hipLaunchKernelGGL((runs_apply_kernel<float, false>), grid, block, 0, stream, wf, state,
+                         p.M, p.Z, ntiles, k0, v0, starts, payload, lr, eps);
+  }
   return hipGetLastError();
 }
 

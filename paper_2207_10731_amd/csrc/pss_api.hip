@@ -112,6 +112,20 @@ bool by_address_auto(int64_t M, const KParams& p) {
          p.N * static_cast<int64_t>(p.d) < (1ll << 31);
 }
 
+// Chunks of at least this many elements deposit by address as run sums
+// (grouped by token first): a run's chunk is then a read of whole lines.
+constexpr uint32_t kRunsMinZ = 64;
+bool runs_fit(const KParams& p) {
+  return p.Z >= kRunsMinZ && p.N * static_cast<int64_t>(p.C) < (1ll << 31) &&
+         p.N * static_cast<int64_t>(p.d) < (1ll << 31);
+}
+// AUTO never picks them: with chunks that long the atomics move whole lines
+// at the memory system's streaming rate, and writing the run sums out and
+// reading them back costs as much (row-hash workload: backward 1.66 ms
+// against 1.11-1.23 ms).  Asked for with the flag they give the same update
+// with every sum taken in a fixed order: the result does not change from
+// run to run.
+
 hipError_t pool_for_current_device(hipMemPool_t* out) {
   int dev = 0;
   hipError_t st = hipGetDevice(&dev);
@@ -364,7 +378,8 @@ int hip_status(hipError_t st) { return st == hipSuccess ? PSS_OK : PSS_ERR_HIP; 
 bool groups_by_token(int64_t M, const KParams& p, const pss_hash_params* hp) {
   const uint32_t variant = hp->flags & PSS_BWD_MASK;
   if (variant != PSS_BWD_AUTO && variant != PSS_BWD_SORTED) return false;
-  if (hp->flags & PSS_DEPOSIT_BY_ADDRESS) return false;
+  // by address: grouped only as run sums (chunks of 64 elements or more)
+  if (hp->flags & PSS_DEPOSIT_BY_ADDRESS) return p.Z >= kRunsMinZ;
   return !(variant == PSS_BWD_AUTO && by_address_auto(M, p));
 }
 
@@ -373,10 +388,12 @@ struct BackwardPlan {
   KParams p;
   uint32_t variant = PSS_BWD_SORTED;  // ATOMIC, SORTED or SPARSE
   bool by_address = false;            // SORTED: records sorted by address tile
+  bool runs = false;                  // ... the records being run sums (grouped by token)
   bool bf16 = false;
   bool fused = false;   // SGD on float32 storage: deposits go into `shared`
   size_t g_bytes = 0;   // float32 gradient buffer (unfused updates), 256-aligned
-  size_t ws_bytes = 0;  // grouping (SORTED) or sparse workspace, after it
+  size_t runs_bytes = 0;  // run sums by address: records and payload, after G
+  size_t ws_bytes = 0;  // grouping (SORTED) or sparse workspace, after those
 };
 constexpr int kNothingToDo = -1;  // no lookups: G == 0, nothing changes
 
@@ -401,11 +418,13 @@ int plan_backward(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
   if (addr_asked && (variant == PSS_BWD_ATOMIC || variant == PSS_BWD_SPARSE))
     return PSS_ERR_UNSUPPORTED;
   if (addr_asked && p.N * static_cast<int64_t>(p.d) >= (1ll << 31)) return PSS_ERR_UNSUPPORTED;
+  if (addr_asked && p.Z >= kRunsMinZ && !runs_fit(p)) return PSS_ERR_UNSUPPORTED;
   if (p.N == 0) return kNothingToDo;
   const bool auto_pick = variant == PSS_BWD_AUTO;
   if (auto_pick) variant = auto_variant(M, p, state != nullptr || plan->bf16, sparse_fits);
   plan->variant = variant;
   plan->by_address = variant == PSS_BWD_SORTED && (addr_asked || (auto_pick && by_address_auto(M, p)));
+  plan->runs = plan->by_address && p.Z >= kRunsMinZ;
   if (variant == PSS_BWD_SPARSE) {
     // Alg. 1 sparse branch: 256 bytes for the unique count, then its workspace
     plan->ws_bytes = 256 + pss::sparse_workspace_bytes(p);
@@ -414,6 +433,12 @@ int plan_backward(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
   // SGD on float32 storage is linear in G: deposit -lr * grad directly into
   // the shared array.  Otherwise deposit G into a scratch buffer first.
   plan->fused = state == nullptr && !plan->bf16;
+  if (plan->runs) {
+    // the tiles update `shared` (and `state`) directly: no G buffer
+    plan->runs_bytes = (pss::runs_workspace_bytes(p) + 255) & ~size_t(255);
+    plan->ws_bytes = pss::sorted_workspace_bytes(p);
+    return PSS_OK;
+  }
   plan->g_bytes = plan->fused ? 0 : (static_cast<size_t>(M) * sizeof(float) + 255) & ~size_t(255);
   plan->ws_bytes = variant != PSS_BWD_SORTED ? 0
                    : plan->by_address       ? pss::addr_workspace_bytes(p)
@@ -422,7 +447,7 @@ int plan_backward(void* shared, float* state, int64_t M, int32_t Z, int32_t d,
 }
 
 // Enqueues the planned backward on `stream`.  ws: scratch of at least
-// plan.g_bytes + plan.ws_bytes bytes; prep: a grouping made ahead for this
+// plan.g_bytes + plan.runs_bytes + plan.ws_bytes bytes; prep: a grouping made ahead for this
 // batch (SORTED only), or null.
 hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state, float eps,
                             const void* indices, const void* offsets, const void* grad_out,
@@ -433,6 +458,23 @@ hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state
     uint32_t* count = static_cast<uint32_t*>(ws);
     return pss::launch_sparse_update(p, indices, offsets, grad_out, static_cast<char*>(ws) + 256,
                                      count, shared, plan.bf16, state, lr, eps, stream);
+  }
+  if (plan.runs) {
+    void* runs_ws = static_cast<char*>(ws) + plan.g_bytes;
+    void* group_ws = static_cast<char*>(runs_ws) + plan.runs_bytes;
+    pss::GroupedPairs pairs;
+    hipError_t e = hipSuccess;
+    if (prep != nullptr) {
+      // the grouping ran on the library stream during the forward
+      e = hipStreamWaitEvent(stream, prep->ready, 0);
+      pairs = prep->pairs;
+    } else {
+      e = pss::launch_group_sorted(p, indices, offsets, group_ws, stream, &pairs);
+    }
+    if (e == hipSuccess)
+      e = pss::launch_deposit_runs(shared, plan.bf16, state, lr, eps, p, pairs, grad_out, runs_ws,
+                                   stream);
+    return e;
   }
   float* dst = plan.fused ? static_cast<float*>(shared) : static_cast<float*>(ws);
   void* sort_ws = static_cast<char*>(ws) + plan.g_bytes;
@@ -563,13 +605,14 @@ int pss_backward_update(void* shared, float* state, int64_t M, int32_t Z, int32_
   if (st != PSS_OK) return st == kNothingToDo ? PSS_OK : st;
   std::unique_lock<std::mutex> prep_lock;
   Prepared* prep = take_prepared(stream, indices, offsets, plan.p,
-                                 plan.variant == PSS_BWD_SORTED && !plan.by_address &&
-                                     !capturing(stream),
+                                 plan.variant == PSS_BWD_SORTED &&
+                                     (!plan.by_address || plan.runs) && !capturing(stream),
                                  &prep_lock);
   if (prep != nullptr) plan.ws_bytes = 0;  // the grouping is already made
   CallScratch scratch;
-  if (plan.g_bytes + plan.ws_bytes > 0) {
-    const int ts = scratch.take(plan.g_bytes + plan.ws_bytes, stream);
+  const size_t need = plan.g_bytes + plan.runs_bytes + plan.ws_bytes;
+  if (need > 0) {
+    const int ts = scratch.take(need, stream);
     if (ts != PSS_OK) return ts;
   }
   const hipError_t e = enqueue_backward(plan, shared, state, hash_params->eps, indices, offsets,
@@ -586,9 +629,10 @@ int pss_backward_update_noalloc(void* shared, float* state, int64_t M, int32_t Z
   const int st = plan_backward(shared, state, M, Z, d, hash_params, indices, offsets, grad_out, lr,
                                &plan);
   if (st != PSS_OK) return st == kNothingToDo ? PSS_OK : st;
-  if (plan.g_bytes + plan.ws_bytes > kStaticScratchBytes) return PSS_ERR_SCRATCH_LIMIT;
+  const size_t need = plan.g_bytes + plan.runs_bytes + plan.ws_bytes;
+  if (need > kStaticScratchBytes) return PSS_ERR_SCRATCH_LIMIT;
   void* ws = nullptr;
-  if (plan.g_bytes + plan.ws_bytes > 0 && static_scratch_for_current_device(&ws) != hipSuccess)
+  if (need > 0 && static_scratch_for_current_device(&ws) != hipSuccess)
     return PSS_ERR_HIP;
   return enqueue_backward(plan, shared, state, hash_params->eps, indices, offsets, grad_out, lr, ws,
                           nullptr, stream) == hipSuccess

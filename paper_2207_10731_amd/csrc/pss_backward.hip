@@ -162,27 +162,6 @@ hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, cons
 // arithmetic; bfloat16 storage is widened exactly and rounded once (RNE).
 // ---------------------------------------------------------------------------
 
-template <typename WT>
-__device__ __forceinline__ void store_weight(WT* w, int64_t m, float v);
-template <>
-__device__ __forceinline__ void store_weight<float>(float* w, int64_t m, float v) {
-  w[m] = v;
-}
-template <>
-__device__ __forceinline__ void store_weight<uint16_t>(uint16_t* w, int64_t m, float v) {
-  w[m] = f32_to_bf16_rne(v);
-}
-template <typename WT>
-__device__ __forceinline__ float load_weight64(const WT* w, int64_t m);
-template <>
-__device__ __forceinline__ float load_weight64<float>(const float* w, int64_t m) {
-  return w[m];
-}
-template <>
-__device__ __forceinline__ float load_weight64<uint16_t>(const uint16_t* w, int64_t m) {
-  return bf16_to_f32(w[m]);
-}
-
 template <typename WT, bool ADAGRAD>
 __global__ __launch_bounds__(kBlockThreads) void optimizer_kernel(
     WT* __restrict__ w, float* __restrict__ s, const float* __restrict__ G, const int64_t M,
@@ -191,17 +170,7 @@ __global__ __launch_bounds__(kBlockThreads) void optimizer_kernel(
   for (int64_t m = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; m < M;
        m += stride) {
     const float g = __builtin_nontemporal_load(G + m);
-    if (g != 0.f) {
-      float upd;
-      if (ADAGRAD) {
-        const float sn = s[m] + g * g;
-        s[m] = sn;
-        upd = lr * g / (sqrtf(sn) + eps);
-      } else {
-        upd = lr * g;
-      }
-      store_weight(w, m, load_weight64(w, m) - upd);
-    }
+    if (g != 0.f) apply_update<WT, ADAGRAD>(w, s, m, g, lr, eps);
   }
 }
 

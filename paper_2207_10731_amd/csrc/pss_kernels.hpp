@@ -95,6 +95,50 @@ __device__ __forceinline__ float load_weight<uint16_t>(const uint16_t* w, uint32
   return bf16_to_f32(w[m]);
 }
 
+template <typename WT>
+__device__ __forceinline__ void store_weight(WT* w, int64_t m, float v);
+template <>
+__device__ __forceinline__ void store_weight<float>(float* w, int64_t m, float v) {
+  w[m] = v;
+}
+template <>
+__device__ __forceinline__ void store_weight<uint16_t>(uint16_t* w, int64_t m, float v) {
+  w[m] = f32_to_bf16_rne(v);
+}
+template <typename WT>
+__device__ __forceinline__ float load_weight64(const WT* w, int64_t m);
+template <>
+__device__ __forceinline__ float load_weight64<float>(const float* w, int64_t m) {
+  return w[m];
+}
+template <>
+__device__ __forceinline__ float load_weight64<uint16_t>(const uint16_t* w, int64_t m) {
+  return bf16_to_f32(w[m]);
+}
+
+// One element's update from its gradient sum g (g != 0): SGD w -= lr * g, or
+// Adagrad s += g^2, w -= lr * g / (sqrt(s) + eps); float32 arithmetic,
+// bfloat16 storage widened exactly and rounded once.
+// The same with the element's weight (widened) and state already loaded.
+template <typename WT, bool ADAGRAD>
+__device__ __forceinline__ void update_loaded(WT* w, float* s, int64_t m, float g, float w_old,
+                                              float s_old, float lr, float eps) {
+  float upd;
+  if (ADAGRAD) {
+    const float sn = s_old + g * g;
+    s[m] = sn;
+    upd = lr * g / (sqrtf(sn) + eps);
+  } else {
+    upd = lr * g;
+  }
+  store_weight(w, m, w_old - upd);
+}
+template <typename WT, bool ADAGRAD>
+__device__ __forceinline__ void apply_update(WT* w, float* s, int64_t m, float g, float lr,
+                                             float eps) {
+  update_loaded<WT, ADAGRAD>(w, s, m, g, load_weight64(w, m), ADAGRAD ? s[m] : 0.f, lr, eps);
+}
+
 __device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
   return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), lane));
 }

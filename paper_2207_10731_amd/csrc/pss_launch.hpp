@@ -86,6 +86,21 @@ hipError_t launch_deposit_addr(float* dst, bool assign, float scale, const KPara
                                const void* indices, const void* offsets, const void* grad,
                                void* workspace, hipStream_t stream);
 
+// Run sums by address: with the lookups grouped by token (g), every run
+// sum becomes one record per chunk, the records are radix-sorted by address
+// tile and each tile applies SGD or Adagrad (state != nullptr) to its
+// elements directly; w is float32 or bfloat16 storage.  Requires Z >= 1,
+// Z <= 4096 and p.N * p.C < 2^31.  workspace: runs_workspace_bytes(p).
+size_t runs_workspace_bytes(const KParams& p);
+hipError_t launch_deposit_runs(void* w, bool bf16, float* state, float lr, float eps,
+                               const KParams& p, const GroupedPairs& g, const void* grad,
+                               void* workspace, hipStream_t stream);
+// The reduce stage writing records instead of depositing: payload rows
+// (N x d floats), record keys and slots (N * C each).
+hipError_t launch_reduce_records(float* payload, float scale, const KParams& p,
+                                 const GroupedPairs& g, const void* grad, uint32_t* rkey,
+                                 uint32_t* rval, hipStream_t stream);
+
 // Dense optimizer pass over the M elements of a gradient buffer G (G[m] == 0
 // leaves element m untouched).  state == nullptr selects SGD.
 hipError_t launch_optimizer(void* w, bool bf16, float* state, const float* G, int64_t M, float lr,

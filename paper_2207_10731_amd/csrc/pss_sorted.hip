@@ -544,10 +544,15 @@ __device__ __forceinline__ void load_rows(float (&g)[U][EPL], const GT* __restri
 // goes to the buffer (values, key), except the quarter's first run while
 // `head` is set (it continues a run of the previous quarter): that one goes
 // to headv and clears `head`.  Returns the number of runs put in the buffer.
-template <int EPL, int U>
+//
+// With REC the merged position of each buffered run's first pair goes to
+// rst[] (run_start: first position of the run in progress, updated as runs
+// end; q0 is the quarter's first position in the piece).
+template <int EPL, int U, bool REC = false>
 __device__ __forceinline__ int sum_runs(const float (&g)[U][EPL], float* acc, uint32_t wk, int q,
                                         int nq, uint32_t after, float* vals, uint32_t* rkeys,
-                                        bool& head, float* headv, int lane) {
+                                        bool& head, float* headv, int lane, uint32_t* rst = nullptr,
+                                        uint32_t* run_start = nullptr, int q0 = 0) {
   int nrun = 0;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -566,9 +571,13 @@ __device__ __forceinline__ int sum_runs(const float (&g)[U][EPL], float* acc, ui
         if (head) {
           head = false;
         } else {
-          if (lane == 0) rkeys[nrun] = h;
+          if (lane == 0) {
+            rkeys[nrun] = h;
+            if (REC) rst[nrun] = *run_start;
+          }
           ++nrun;
         }
+        if (REC) *run_start = static_cast<uint32_t>(q0 + q + u + 1);
       }
     }
   }
@@ -594,11 +603,43 @@ __device__ __forceinline__ void deposit_run(float* __restrict__ dst, float scale
   }
 }
 
-template <int EPL, int U, bool SIGN, typename GT>
+// Record form of deposit_run: the lane's EPL values of the run, scaled and
+// signed per chunk (0 for a chunk that is not read), become row `slot_row`
+// of the payload array (d floats per row).
+template <int EPL, bool SIGN>
+__device__ __forceinline__ void record_run(float* __restrict__ payload, float scale,
+                                           const KParams& p, uint32_t h, uint64_t slot_row,
+                                           const float* v, const bool* act, const uint32_t* step,
+                                           const uint32_t* step2, const uint32_t* kk,
+                                           uint32_t c0, int lane) {
+  const uint32_t h20 = SIGN ? sign_hash0(h, p.s_alpha, p.s_beta) : 0u;
+#pragma unroll
+  for (int r = 0; r < EPL; ++r) {
+    if (!act[r]) continue;
+    float x = scale * v[r];
+    if (SIGN) {
+      const uint32_t ent = chunk_entry<SIGN>(fast_mod(add_mod_p(h, step[r]), p.fm_c, p.M),
+                                             add_mod_p(h20, step2[r]), p);
+      x = apply_sign(x, elem_of<SIGN>(ent, kk[r], p.M));
+    }
+    payload[slot_row * p.d + c0 + lane + kWave * r] = x;
+  }
+}
+
+// Without REC: the reduce-and-deposit kernel described above (dst, scale).
+// With REC (run sums deposited by address): no atomics; every run of the
+// piece becomes one record per chunk, slot (p0 + i) * C + j for the run's
+// first merged position i and chunk j: payload row p0 + i holds the run's
+// scaled, signed sum (dst is the payload array, N x d floats), rkey[slot] the
+// chunk's base (kNoRecord for a chunk that is not read and for every
+// position that starts no run), rval[slot] = slot.
+constexpr uint32_t kNoRecord = 0xffffffffu;
+template <int EPL, int U, bool SIGN, typename GT, bool REC>
 __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
     float* __restrict__ dst, const float scale, const KParams p,
     const uint32_t* __restrict__ keys, const uint32_t* __restrict__ rows,
-    const GT* __restrict__ grad, const float* __restrict__ inv_len, const int64_t n) {
+    const GT* __restrict__ grad, const float* __restrict__ inv_len, const int64_t n,
+    uint32_t* __restrict__ rkey, uint32_t* __restrict__ rval) {
   static_assert(U * kWave * EPL == kSlotFloats, "a buffer holds U run sums");
   const int lane = threadIdx.x & (kWave - 1);
   const int w = static_cast<int>(__builtin_amdgcn_readfirstlane(threadIdx.x >> 6));
@@ -627,6 +668,8 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
   __shared__ int nruns[kReaders][2];
   __shared__ uint32_t qkey[kReaders];  // key at the start of each quarter
   __shared__ int qflags[kReaders];     // bit 0: tail open, bit 1: through (no run ends inside)
+  __shared__ uint32_t rst[kReaders][2][REC ? U : 1];  // REC: first position of each buffered run
+  __shared__ uint32_t lastst[kReaders];               // REC: first position of the open run
 
   bool act[EPL];
 #pragma unroll
@@ -677,10 +720,30 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
       after = mk[q0 + nq];  // the run goes on past the quarter
     }
     if (lane == 0) qkey[pair] = mk[q0];
+    if (REC && blockIdx.y == 0 && lane < nq) {
+      // a run starts here when the key differs from the previous position's
+      const bool starts = my == 0 || mk[my] != mk[my - 1];
+      const uint32_t h20 = SIGN ? sign_hash0(wk, p.s_alpha, p.s_beta) : 0u;
+      uint32_t step = 0, step2 = 0;
+      for (uint32_t j = 0; j < p.C; ++j) {
+        const uint64_t slot = static_cast<uint64_t>(p0 + my) * p.C + j;
+        uint32_t key = kNoRecord;
+        if (starts) {
+          const uint32_t ent = chunk_entry<SIGN>(fast_mod(add_mod_p(wk, step), p.fm_c, p.M),
+                                                 add_mod_p(h20, step2), p);
+          if (ent != kSkip) key = ent & 0x7fffffffu;
+        }
+        rkey[slot] = key;
+        rval[slot] = static_cast<uint32_t>(slot);
+        step = add_mod_p(step, p.a);
+        if (SIGN) step2 = add_mod_p(step2, p.a2);
+      }
+    }
   }
   lds_barrier();  // every reader holds its quarter: the sort buffers are free
   if (reader && nq > 0) {
     bool head = head_open;
+    uint32_t run_start = static_cast<uint32_t>(q0);
     float acc[EPL];
 #pragma unroll
     for (int r = 0; r < EPL; ++r) acc[r] = 0.f;
@@ -700,10 +763,12 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
         int nr = 0;
         float* hv = headv + pair * kRowF;
         if (q < nq)
-          nr = (k & 1) ? sum_runs<EPL, U>(gb, acc, wk, q, nq, after, vals[pair][k & 1],
-                                          rkeys[pair][k & 1], head, hv, lane)
-                       : sum_runs<EPL, U>(ga, acc, wk, q, nq, after, vals[pair][k & 1],
-                                          rkeys[pair][k & 1], head, hv, lane);
+          nr = (k & 1) ? sum_runs<EPL, U, REC>(gb, acc, wk, q, nq, after, vals[pair][k & 1],
+                                               rkeys[pair][k & 1], head, hv, lane,
+                                               rst[pair][k & 1], &run_start, q0)
+                       : sum_runs<EPL, U, REC>(ga, acc, wk, q, nq, after, vals[pair][k & 1],
+                                               rkeys[pair][k & 1], head, hv, lane,
+                                               rst[pair][k & 1], &run_start, q0);
         if (lane == 0) nruns[pair][k & 1] = nr;
       } else {
         // the open run's part in this quarter (with no run ending inside,
@@ -712,7 +777,10 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
 #pragma unroll
           for (int r = 0; r < EPL; ++r) tailv[pair * kRowF + kWave * r + lane] = acc[r];
         }
-        if (lane == 0) qflags[pair] = (tail_open ? 1 : 0) | (head ? 2 : 0);
+        if (lane == 0) {
+          qflags[pair] = (tail_open ? 1 : 0) | (head ? 2 : 0);
+          if (REC) lastst[pair] = run_start;
+        }
       }
       lds_barrier();
     }
@@ -742,7 +810,12 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
           float v[EPL];
 #pragma unroll
           for (int r = 0; r < EPL; ++r) v[r] = vals[pair][b][s * kRowF + kWave * r + lane];
-          deposit_run<EPL, SIGN>(dst, scale, p, rkeys[pair][b][s], v, act, step, step2, kk);
+          if (REC)
+            record_run<EPL, SIGN>(dst, scale, p, rkeys[pair][b][s],
+                                  static_cast<uint64_t>(p0) + rst[pair][b][s], v, act, step,
+                                  step2, kk, c0, lane);
+          else
+            deposit_run<EPL, SIGN>(dst, scale, p, rkeys[pair][b][s], v, act, step, step2, kk);
         }
       }
       lds_barrier();
@@ -764,7 +837,11 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_deposit_kernel(
       }
 #pragma unroll
       for (int r = 0; r < EPL; ++r) v[r] += headv[q * kRowF + kWave * r + lane];
-      deposit_run<EPL, SIGN>(dst, scale, p, qkey[q], v, act, step, step2, kk);
+      if (REC)
+        record_run<EPL, SIGN>(dst, scale, p, qkey[q], static_cast<uint64_t>(p0) + lastst[pair], v,
+                              act, step, step2, kk, c0, lane);
+      else
+        deposit_run<EPL, SIGN>(dst, scale, p, qkey[q], v, act, step, step2, kk);
     }
   }
 }
@@ -849,34 +926,38 @@ hipError_t launch_keygen(const KParams& p, const void* indices, const void* offs
   return hipGetLastError();
 }
 
-template <int EPL, int U, bool SIGN, typename GT>
+template <int EPL, int U, bool SIGN, typename GT, bool REC>
 static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const GT* grad, const float* inv_len,
-                                  hipStream_t stream) {
+                                  uint32_t* rkey, uint32_t* rval, hipStream_t stream) {
   const uint64_t blocks = (static_cast<uint64_t>(p.N) + kPiece - 1) / kPiece;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
-  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT>),
+  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT, REC>),
                      dim3(static_cast<uint32_t>(blocks), slabs), dim3(kReduceThreads), 0, stream,
-                     dst, scale, p, keys, rows, grad, inv_len, p.N);
+                     dst, scale, p, keys, rows, grad, inv_len, p.N, rkey, rval);
   return hipGetLastError();
 }
 
-template <bool SIGN, typename GT>
+template <bool SIGN, typename GT, bool REC>
 static hipError_t launch_reduce_s(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const GT* grad, const float* il,
-                                  hipStream_t stream) {
-  if (p.d <= 64) return launch_reduce_t<1, 16, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  if (p.d <= 128) return launch_reduce_t<2, 8, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  if (p.d <= 256) return launch_reduce_t<4, 4, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
-  return launch_reduce_t<8, 2, SIGN>(dst, scale, p, keys, rows, grad, il, stream);
+                                  uint32_t* rk, uint32_t* rv, hipStream_t stream) {
+  if (p.d <= 64)
+    return launch_reduce_t<1, 16, SIGN, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
+  if (p.d <= 128)
+    return launch_reduce_t<2, 8, SIGN, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
+  if (p.d <= 256)
+    return launch_reduce_t<4, 4, SIGN, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
+  return launch_reduce_t<8, 2, SIGN, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
 }
 
-template <typename GT>
+template <typename GT, bool REC>
 static hipError_t launch_reduce_g(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const GT* grad, const float* il,
-                                  hipStream_t stream) {
-  if (p.sign_mode) return launch_reduce_s<true>(dst, scale, p, keys, rows, grad, il, stream);
-  return launch_reduce_s<false>(dst, scale, p, keys, rows, grad, il, stream);
+                                  uint32_t* rk, uint32_t* rv, hipStream_t stream) {
+  if (p.sign_mode)
+    return launch_reduce_s<true, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
+  return launch_reduce_s<false, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
 }
 
 hipError_t launch_group_sorted(const KParams& p, const void* indices, const void* offsets,
@@ -923,10 +1004,25 @@ hipError_t launch_reduce_sorted(float* dst, float scale, const KParams& p, const
                                 const void* grad, hipStream_t stream) {
   if (p.N == 0) return hipSuccess;
   if (p.rows_bf16)
-    return launch_reduce_g(dst, scale, p, g.keys, g.rows, static_cast<const uint16_t*>(grad),
-                           g.inv_len, stream);
-  return launch_reduce_g(dst, scale, p, g.keys, g.rows, static_cast<const float*>(grad), g.inv_len,
-                         stream);
+    return launch_reduce_g<uint16_t, false>(dst, scale, p, g.keys, g.rows,
+                                            static_cast<const uint16_t*>(grad), g.inv_len, nullptr,
+                                            nullptr, stream);
+  return launch_reduce_g<float, false>(dst, scale, p, g.keys, g.rows,
+                                       static_cast<const float*>(grad), g.inv_len, nullptr,
+                                       nullptr, stream);
+}
+
+hipError_t launch_reduce_records(float* payload, float scale, const KParams& p,
+                                 const GroupedPairs& g, const void* grad, uint32_t* rkey,
+                                 uint32_t* rval, hipStream_t stream) {
+  if (p.N == 0) return hipSuccess;
+  if (p.rows_bf16)
+    return launch_reduce_g<uint16_t, true>(payload, scale, p, g.keys, g.rows,
+                                           static_cast<const uint16_t*>(grad), g.inv_len, rkey,
+                                           rval, stream);
+  return launch_reduce_g<float, true>(payload, scale, p, g.keys, g.rows,
+                                      static_cast<const float*>(grad), g.inv_len, rkey, rval,
+                                      stream);
 }
 
 hipError_t launch_deposit_sorted(float* dst, float scale, const KParams& p, const void* indices,

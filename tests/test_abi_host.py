@@ -279,3 +279,26 @@ def test_noalloc_rejects_bad_arguments_and_oversized_calls(lib):
     hp0 = pss.pss_hash_params(5, 7, 26, 262144, 0, 0, 1e-10, 0)
     assert f(dummy, None, 2_500_000, 32, 128, ctypes.byref(hp0), dummy, dummy, dummy,
              ctypes.c_float(0.1), None) == pss.PSS_OK
+
+
+def test_by_address_flag_rules(lib):
+    """PSS_DEPOSIT_BY_ADDRESS is refused with ATOMIC or SPARSE and beyond
+    2^31 (lookup, dim) records, on the host before anything is enqueued; the
+    run-sum form's scratch (N x d floats of run sums) counts against the
+    allocation-free entry point's limit."""
+    dummy = ctypes.c_void_p(0x1000)
+    f = lib.pss_backward_update
+    A = pss.PSS_DEPOSIT_BY_ADDRESS
+    for variant in (pss.PSS_BWD_ATOMIC, pss.PSS_BWD_SPARSE):
+        hp = pss.pss_hash_params(5, 7, 4, 2, 8, 0, 1e-10, variant | A)
+        assert f(dummy, None, 4096, 4, 16, ctypes.byref(hp), dummy, dummy, dummy,
+                 ctypes.c_float(0.1), None) == pss.PSS_ERR_UNSUPPORTED
+    for Z in (1, 128):  # single contributions, run sums
+        big = pss.pss_hash_params(5, 7, 1, 2**24, 2**24, 0, 1e-10, pss.PSS_BWD_SORTED | A)
+        assert f(dummy, None, 2_500_000, Z, 128, ctypes.byref(big), dummy, dummy, dummy,
+                 ctypes.c_float(0.1), None) == pss.PSS_ERR_UNSUPPORTED
+    # run sums of 200 K whole-row lookups: 102 MB of run sums, beyond 64 MiB
+    runs = pss.pss_hash_params(5, 7, 1, 200_000, 200_000, 0, 1e-10, pss.PSS_BWD_SORTED | A)
+    assert lib.pss_backward_update_noalloc(dummy, dummy, 2_500_000, 128, 128, ctypes.byref(runs),
+                                           dummy, dummy, dummy, ctypes.c_float(0.1),
+                                           None) == pss.PSS_ERR_SCRATCH_LIMIT

@@ -43,8 +43,9 @@
  *   PSS_INDEX_I32  indices and offsets are int32.
  *   PSS_ROWS_BF16  out is written, and grad_out read, as bfloat16 (out is
  *     rounded to nearest even from the float32 result).
- *   PSS_DEPOSIT_BY_ADDRESS  with the SORTED variant (or AUTO): the deposit
- *     is ordered by address instead of made with float atomics to memory.
+ *   PSS_DEPOSIT_BY_ADDRESS  with the SORTED variant (with AUTO: whenever
+ *     AUTO picks SORTED): the deposit is ordered by address instead of made
+ *     with float atomics to memory.
  *     The contributions are radix-sorted by address tile (2^14 elements)
  *     and each tile sums its contributions on chip and is updated once.
  *     - Z < 64: every (lookup, dim) contribution is its own (address, value)

@@ -29,8 +29,11 @@
 // radix-sorted by the tile of their base, and one workgroup per tile sums
 // the payloads of every chunk that reaches the tile (its own, the previous
 // tile's spilling over the boundary and, for tile 0, those wrapping past M)
-// in LDS, then applies SGD or Adagrad to the tile's elements in place: no
-// float atomics to memory, no G buffer, no dense optimizer pass.
+// in LDS, each wavefront owning a range of the tile and adding in record
+// order, then applies SGD or Adagrad to the tile's elements in place: no
+// atomics at all, no G buffer, no dense optimizer pass, and every sum taken
+// in a fixed order (the update is bit-identical run to run).  Opt-in: with
+// chunks this long the atomic deposit moves whole lines and is faster.
 #include "pss_launch.hpp"
 
 namespace pss {

@@ -12,7 +12,10 @@ gradient (pss_gradient_sparse) on the workloads whose arrays fit the export:
 its location count equals the number of distinct elements the batch reads
 (the union of the oracle's chunk windows), its locations ascend strictly,
 every sampled element the batch reads is listed with the oracle's value, and
-no sampled element it does not read is listed."""
+no sampled element it does not read is listed.
+
+The run sums by address (opt-in, whole-row chunks) at full size on the
+row-hash workload, with and without the prepared grouping: bit-identical."""
 import numpy as np
 import pytest
 import torch
@@ -214,3 +217,30 @@ def test_fullsize_gradient_sparse(key):
     got = vals[pos[listed]]
     err = np.abs(got - G[listed])
     assert np.all(err <= 1e-5 * A[listed] + 1e-30), f"{(err > 1e-5 * A[listed]).sum()} values off"
+
+
+def test_fullsize_runs_by_address():
+    """Run sums by address on the row-hash workload at full size (its chunks
+    are whole rows, Z = 128): the prepared step, sampled elements as above,
+    and the same update repeated from the same state bit-identical."""
+    flags = pss.PSS_BWD_SORTED | pss.PSS_DEPOSIT_BY_ADDRESS | pss.PSS_PREPARE_BACKWARD
+    F = Full("c5", flags=flags)
+    wl = F.wl
+    g, grad = _grad(F)
+    out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=F.dev)
+    w0, s0 = F.shared.clone(), F.state.clone()
+    print(f"full-size c5: run sums by address over {F.x.N} lookups", flush=True)
+    pss.pss_forward(F.shared, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, out)
+    pss.pss_backward_update(F.shared, F.state, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, wl.lr)
+    torch.cuda.synchronize()
+    w1, s1 = F.shared.clone(), F.state.clone()
+    # again from the same state, without the prepared grouping
+    F.shared.copy_(w0)
+    F.state.copy_(s0)
+    F.hp.flags = pss.PSS_BWD_SORTED | pss.PSS_DEPOSIT_BY_ADDRESS
+    pss.pss_backward_update(F.shared, F.state, wl.M, wl.Z, wl.d, F.hp, F.idx, F.off, g, wl.lr)
+    torch.cuda.synchronize()
+    assert torch.equal(F.shared.view(torch.int16), w1.view(torch.int16))
+    assert torch.equal(F.state.view(torch.int32), s1.view(torch.int32))
+    del g, w0, s0, w1, s1, out
+    _check_backward(F, grad)

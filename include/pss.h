@@ -52,10 +52,11 @@
  *       record; the tile is applied to the array (SGD on float32) or stored
  *       as that tile of the float32 gradient buffer before the optimizer
  *       pass.  16 B of scratch per (lookup, dim).  AUTO takes this by itself
- *       for chunks shorter than a 64-byte memory line (Z < 16) on an array
- *       beyond the memory-side cache (M * 4 > 256 MiB), where lookups seldom
- *       repeat and each contribution would otherwise be an atomic to its
- *       own line.
+ *       for chunks of at most 2 elements (Z <= 2) on an array beyond the
+ *       memory-side cache (M * 4 > 256 MiB), where lookups seldom repeat
+ *       and each contribution would otherwise be an atomic to its own line;
+ *       from Z = 4 on, the grouped deposit's one atomic per chunk costs
+ *       less than sorting every (lookup, dim) record.
  *     - Z >= 64: the lookups are grouped by token first (as SORTED does) and
  *       each run sum becomes one record per chunk (Z values); each tile adds
  *       the chunks reaching it in a fixed order and applies the optimizer to

@@ -102,13 +102,19 @@ uint32_t auto_variant(int64_t M, const KParams& p, bool unfused, bool sparse_fit
   return PSS_BWD_SORTED;
 }
 
-// AUTO's deposit order for the SORTED variant: by address when a chunk is
-// shorter than a 64-byte memory line and the array lies beyond the
-// memory-side cache (M * 4 > 256 MiB).  There lookups seldom repeat, so
-// grouping by token removes nothing, and each contribution would be a float
-// atomic to its own line.  Needs N * d < 2^31 records.
+// AUTO's deposit order for the SORTED variant: by address when a chunk has
+// at most 2 elements and the array lies beyond the memory-side cache
+// (M * 4 > 256 MiB, where tables are large and lookups seldom repeat).
+// The address sort costs the same for every Z (it moves N * d records);
+// grouping by token leaves one atomic per lookup and chunk when tokens do
+// not repeat.  Measured on a 26-table one-hot batch of uniform indices
+// (4 GB array): Z = 1 12.8 -> 5.7 ms, Z = 2 6.7 -> 5.6 ms by address, but
+// Z = 4 3.7 against 5.4 ms and Z = 8 2.2 against 5.3 ms by token.  Skewed
+// tokens make the grouping cheaper still, hence the array-size condition.
+// Needs N * d < 2^31 records.
+constexpr uint32_t kAddrMaxZ = 2;
 bool by_address_auto(int64_t M, const KParams& p) {
-  return p.Z * sizeof(float) < 64 && M * static_cast<int64_t>(sizeof(float)) > (256ll << 20) &&
+  return p.Z <= kAddrMaxZ && M * static_cast<int64_t>(sizeof(float)) > (256ll << 20) &&
          p.N * static_cast<int64_t>(p.d) < (1ll << 31);
 }
 

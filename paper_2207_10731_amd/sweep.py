@@ -14,6 +14,11 @@ observations).  This module measures the same sweeps here:
                                                   table (Sec. 2.4): time per
                                                   backward variant and the
                                                   empirical eps of Def. 2
+  python -m paper_2207_10731_amd.sweep address    SORTED backward grouped by
+                                                  token vs deposited by
+                                                  address, vs Z and |M|, on a
+                                                  26-table one-hot batch of
+                                                  uniform indices
 
 Inputs: n = 10^7 rows, one uniform index per sample, grad_out = 1.
 Each point: median of `--reps` timed calls (HIP events on the stream the
@@ -139,15 +144,47 @@ def compress_sweep(reps, Z=32):
         del eps, e_sorted, out
 
 
+def address_sweep(reps, tables=26, batch=65536, rows=40_000_000):
+    """Backward (SGD on float32, N(0, 1) output gradient) of a one-hot batch
+    of `tables` tables x `batch` samples with uniform indices over `rows`
+    rows: the SORTED variant grouped by token against the same with
+    PSS_DEPOSIT_BY_ADDRESS, for chunk sizes 1..16 and two array sizes."""
+    rng = np.random.default_rng(5)
+    n = tables * batch
+    idx = torch.from_numpy(rng.integers(0, rows, n, dtype=np.int64)).cuda()
+    off = torch.arange(n + 1, dtype=torch.int64, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(6)
+    grad = torch.randn((batch, tables * DIM), device="cuda", generator=g)
+    print("| M | Z | by token us | by address us |")
+    print("|---|---|---|---|")
+    for M in (2_500_000, 1_000_000_000):
+        w = torch.zeros(M, device="cuda")
+        for Z in (1, 2, 4, 8, 16):
+            t = {}
+            for name, fl in (("token", pss.PSS_BWD_SORTED),
+                             ("address", pss.PSS_BWD_SORTED | pss.PSS_DEPOSIT_BY_ADDRESS)):
+                hp = pss.make_hash_params(9, num_tables=tables, batch=batch, num_indices=n,
+                                          flags=fl)
+                t[name] = _time(lambda: pss.pss_backward_update(w, None, M, Z, DIM, hp, idx, off,
+                                                                grad, 0.1), reps, 2)
+            print(f"| {M} | {Z} | {t['token']:.0f} | {t['address']:.0f} |", flush=True)
+        del w
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["chunk", "crossover", "compress"])
+    ap.add_argument("mode", choices=["chunk", "crossover", "compress", "address"])
     ap.add_argument("--reps", type=int, default=20)
     a = ap.parse_args(argv)
     assert torch.cuda.is_available(), "the sweep needs a GPU"
-    print(f"<!-- {torch.cuda.get_device_name(0)}; n = {ROWS} rows, batch {BATCH}, d = {DIM}, "
-          f"grad_out = 1, median of {a.reps} -->")
-    {"chunk": chunk_sweep, "crossover": crossover_sweep, "compress": compress_sweep}[a.mode](a.reps)
+    if a.mode == "address":
+        print(f"<!-- {torch.cuda.get_device_name(0)}; 26 tables x 65536 samples, one uniform "
+              f"index in [0, 4e7) each, d = {DIM}, grad_out N(0, 1), SGD, median of {a.reps} -->")
+    else:
+        print(f"<!-- {torch.cuda.get_device_name(0)}; n = {ROWS} rows, batch {BATCH}, d = {DIM}, "
+              f"grad_out = 1, median of {a.reps} -->")
+    {"chunk": chunk_sweep, "crossover": crossover_sweep, "compress": compress_sweep,
+     "address": address_sweep}[a.mode](a.reps)
 
 
 if __name__ == "__main__":

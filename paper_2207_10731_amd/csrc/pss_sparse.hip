@@ -15,6 +15,11 @@
 //              sorts last).  With a chunk sign, bit 31 of the record id marks
 //              a -1 chunk and chunks of factor 0 get the sentinel base (they
 //              read nothing, so they own and add nothing).
+//   pre-merge  when the records average 16 or more per base of the array
+//              (N * C >= 16 * M), the records that share a base are summed
+//              once (their signed run-sum pieces, in record order) into one
+//              record per distinct base, so that an element's walk below
+//              meets at most Z records
 //   merge      element m is owned by the last chunk, in base order, whose
 //              span [base, base + Z) covers it.  A chunk that runs past M
 //              wraps to 0: it is also entered, shifted by -M, in front of
@@ -343,7 +348,8 @@ constexpr int kStage = 384;  // records a wavefront stages in LDS
 // (base, id | sign) of record y; the walk stops at the first record whose
 // span ends at or before m, or below record `ylo`.
 template <typename Rec>
-__device__ __forceinline__ float walk_sum(const KParams& p, const float* __restrict__ rs, int64_t m,
+__device__ __forceinline__ float walk_sum(const KParams& p, const float* __restrict__ rs,
+                                          const uint32_t rsC, const uint32_t rsD, int64_t m,
                                           int64_t y0, int64_t ylo, Rec rec_of) {
   const int64_t Z = p.Z;
   float v = 0.f;
@@ -363,8 +369,8 @@ __device__ __forceinline__ float walk_sum(const KParams& p, const float* __restr
 #pragma unroll
     for (int u = 0; u < kWalk; ++u) {
       const uint32_t id = rec[u] & 0x7fffffffu;
-      const uint32_t run = id / p.C, j = id - run * p.C;
-      xv[u] = ok[u] ? rs[static_cast<uint64_t>(run) * p.d + j * p.Z +
+      const uint32_t run = id / rsC, j = id - run * rsC;
+      xv[u] = ok[u] ? rs[static_cast<uint64_t>(run) * rsD + j * p.Z +
                          static_cast<uint32_t>(m - by[u])]
                     : 0.f;
     }
@@ -380,8 +386,8 @@ template <int MODE, typename WT, bool ADAGRAD>
 __global__ __launch_bounds__(kBlockThreads) void emit_kernel(
     const KParams p, const uint32_t* __restrict__ cb, const uint32_t* __restrict__ cv,
     const uint32_t* __restrict__ info, const uint32_t* __restrict__ slot,
-    const uint32_t* __restrict__ total, const float* __restrict__ rs, const EmitList list,
-    const EmitUpdate<WT> upd) {
+    const uint32_t* __restrict__ total, const float* __restrict__ rs, const uint32_t rsC,
+    const uint32_t rsD, const EmitList list, const EmitUpdate<WT> upd) {
   __shared__ int32_t sbase_all[kWavesPerBlock][kStage];
   __shared__ uint32_t srec_all[kWavesPerBlock][kStage];
   int32_t* sbase = sbase_all[threadIdx.x >> 6];
@@ -465,12 +471,12 @@ __global__ __launch_bounds__(kBlockThreads) void emit_kernel(
       if (e >= T) continue;
       float v;
       if (staged) {
-        v = walk_sum(p, rs, m, xr - ymin, 0, [&](int64_t y, int64_t& by, uint32_t& rec) {
+        v = walk_sum(p, rs, rsC, rsD, m, xr - ymin, 0, [&](int64_t y, int64_t& by, uint32_t& rec) {
           by = sbase[y];
           rec = srec[y];
         });
       } else {
-        v = walk_sum(p, rs, m, xr, 0, [&](int64_t y, int64_t& by, uint32_t& rec) {
+        v = walk_sum(p, rs, rsC, rsD, m, xr, 0, [&](int64_t y, int64_t& by, uint32_t& rec) {
           by = el.base(static_cast<uint32_t>(y));
           rec = cv[el.sorted_index(static_cast<uint32_t>(y))];
         });
@@ -488,6 +494,108 @@ __global__ __launch_bounds__(kBlockThreads) void emit_kernel(
   (void)Z;
 }
 
+// ---------------------------------------------------------------------------
+// pre-merge of records that share a base
+// ---------------------------------------------------------------------------
+// Records with one base cover the same Z elements: their signed run-sum
+// pieces are summed once per base (in record order) before the ownership
+// and emit steps, so that an element's walk meets at most Z records however
+// many chunks hash to its neighbourhood.
+constexpr uint32_t kNoBase = 0xffffffffu;
+
+// hd[x] = 1 where record x starts a new base (records before the sentinels).
+__global__ __launch_bounds__(kBlockThreads) void merge_heads_kernel(
+    const uint32_t* __restrict__ cb, const uint32_t* __restrict__ num_runs, const uint32_t C,
+    uint32_t* __restrict__ hd) {
+  const int64_t rc = static_cast<int64_t>(*num_runs) * C;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; x < rc;
+       x += stride) {
+    const uint32_t b = cb[x];
+    hd[x] = b != kNoBase && (x == 0 || cb[x - 1] != b) ? 1u : 0u;
+  }
+}
+
+// After the scan of hd: hpos[u] = position of the u-th head; the records of
+// base u are [hpos[u], hpos[u + 1]), hpos[U] = first sentinel position.
+__global__ __launch_bounds__(kBlockThreads) void merge_positions_kernel(
+    const uint32_t* __restrict__ cb, const uint32_t* __restrict__ num_runs, const uint32_t C,
+    const uint32_t* __restrict__ hd, const uint32_t* __restrict__ num_bases,
+    uint32_t* __restrict__ hpos) {
+  const int64_t rc = static_cast<int64_t>(*num_runs) * C;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlockThreads;
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; x < rc;
+       x += stride) {
+    const uint32_t b = cb[x];
+    const uint32_t prev = x > 0 ? cb[x - 1] : kNoBase;
+    if (b != kNoBase && (x == 0 || prev != b)) hpos[hd[x]] = static_cast<uint32_t>(x);
+    // the end of the last base: the first sentinel, or rc
+    if ((b == kNoBase && (x == 0 || prev != kNoBase)) || (b != kNoBase && x + 1 == rc))
+      hpos[*num_bases] = static_cast<uint32_t>(b == kNoBase ? x : rc);
+  }
+}
+
+// One wavefront per base u: mrs[u * Z + k] = sum over its records of the
+// signed run-sum entry k; mb[u] = base, mv[u] = u.  Record ids are
+// requested 64 at a time and their entries kMergeBatch at a time.
+constexpr int kMergeBatch = 8;
+__global__ __launch_bounds__(kBlockThreads) void merge_sums_kernel(
+    const KParams p, const uint32_t* __restrict__ cb, const uint32_t* __restrict__ cv,
+    const uint32_t* __restrict__ hpos, const uint32_t* __restrict__ num_bases,
+    const float* __restrict__ rs, float* __restrict__ mrs, uint32_t* __restrict__ mb,
+    uint32_t* __restrict__ mv) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t U = *num_bases;
+  const uint64_t nwaves = static_cast<uint64_t>(gridDim.x) * kWavesPerBlock;
+  for (uint64_t u = static_cast<uint64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6); u < U;
+       u += nwaves) {
+    const uint32_t lo = hpos[u], hi = hpos[u + 1];
+    for (uint32_t k0 = 0; k0 < p.Z; k0 += kWave) {
+      const uint32_t k = k0 + lane;
+      float acc = 0.f;
+      for (uint32_t x0 = lo; x0 < hi; x0 += kWave) {
+        const uint32_t nx = hi - x0 < static_cast<uint32_t>(kWave) ? hi - x0 : kWave;
+        const uint32_t myid = static_cast<uint32_t>(lane) < nx ? cv[x0 + lane] : 0u;
+        for (uint32_t q0 = 0; q0 < nx; q0 += kMergeBatch) {
+          float v[kMergeBatch];
+#pragma unroll
+          for (int t = 0; t < kMergeBatch; ++t) {
+            const uint32_t q = q0 + t < nx ? q0 + t : nx - 1;
+            const uint32_t id = readlane_u32(myid, static_cast<int>(q));
+            const uint32_t run = (id & 0x7fffffffu) / p.C, j = (id & 0x7fffffffu) - run * p.C;
+            const float x = k < p.Z ? rs[static_cast<uint64_t>(run) * p.d + j * p.Z + k] : 0.f;
+            v[t] = (id >> 31) ? -x : x;
+          }
+#pragma unroll
+          for (int t = 0; t < kMergeBatch; ++t)
+            if (q0 + t < nx) acc += v[t];
+        }
+      }
+      if (k < p.Z) mrs[u * p.Z + k] = acc;
+    }
+    if (lane == 0) {
+      mb[u] = cb[lo];
+      mv[u] = static_cast<uint32_t>(u);
+    }
+  }
+}
+
+// tail_count for the merged list: U bases, no sentinels.
+__global__ void tail_count_merged_kernel(const KParams p, const uint32_t* __restrict__ mb,
+                                         const uint32_t* __restrict__ num_bases,
+                                         uint32_t* __restrict__ info) {
+  const uint64_t rc = *num_bases;
+  uint64_t lo = 0, hi = rc;
+  const uint32_t lim = p.M - p.Z;
+  while (lo < hi) {
+    const uint64_t mid = (lo + hi) / 2;
+    if (mb[mid] > lim) hi = mid; else lo = mid + 1;
+  }
+  info[0] = static_cast<uint32_t>(rc);
+  info[1] = static_cast<uint32_t>(rc - lo);
+  info[3] = static_cast<uint32_t>(rc + (rc - lo));
+}
+
 __global__ void store_count_kernel(const uint32_t* __restrict__ total, int64_t* __restrict__ out) {
   *out = *total;
 }
@@ -498,6 +606,16 @@ __global__ void store_count_kernel(const uint32_t* __restrict__ total, int64_t* 
 
 // Records have 31-bit ids (bit 31 carries the sign): N*C must stay below 2^31.
 static int64_t record_cap(const KParams& p) { return p.N * static_cast<int64_t>(p.C); }
+
+// Pre-merge when the chunk records average at least 16 per base of the
+// array (N * C >= 16 * M, an upper bound: runs are at most lookups).
+// Measured on post-hoc compression of 10^7 x 128 entries (Z = 32): 1000x
+// 51.6 -> 6.5 ms, 10000x 142 -> 6.1 ms; at 100x (3 records per base) even,
+// at 10x 3.4x slower, and 1.3-2x slower on the benchmark batches (2.7-4.3
+// records per base), whose walks are already short.
+static bool sparse_merges(const KParams& p) {
+  return record_cap(p) >= 16 * static_cast<int64_t>(p.M);
+}
 
 static int base_bits(uint32_t M) {  // smallest multiple of 8 with 2^bits > M
   int bits = 8;
@@ -514,8 +632,13 @@ size_t sparse_workspace_bytes(const KParams& p) {
   s += static_cast<size_t>(N) * p.d * 4 + static_cast<size_t>(N) * 4;  // run sums + keys
   s += static_cast<size_t>(cap) * 16 + radix_scratch_bytes(cap);  // chunk records
   s += static_cast<size_t>(cap2) * 4 + scan_scratch_bytes(cap2) + 16;  // ownership
+  if (sparse_merges(p)) {
+    const int64_t ub = cap < static_cast<int64_t>(p.M) ? cap : static_cast<int64_t>(p.M);
+    s += static_cast<size_t>(cap) * 4 + scan_scratch_bytes(cap) + static_cast<size_t>(cap + 1) * 4 +
+         static_cast<size_t>(ub) * (p.Z + 2) * 4 + 64;  // pre-merge
+  }
   if (p.mean) s += static_cast<size_t>(p.num_bags) * 4;  // 1 / |bag| per pooled row
-  return s + 64 * 16;  // alignment slack
+  return s + 72 * 16;  // alignment slack
 }
 
 template <typename T>
@@ -564,6 +687,7 @@ static uint32_t emit_blocks(int64_t cap2) {
 struct SparseState {
   const uint32_t *cb, *cv, *info, *own;
   const float* rs;
+  uint32_t rsC, rsD;  // record id -> rs entry: (id / rsC) * rsD + (id % rsC) * Z + offset
   int64_t cap2;
 };
 
@@ -592,6 +716,15 @@ static hipError_t sparse_prepare(const KParams& p, const void* indices, const vo
   uint32_t* oscr = carve<uint32_t>(cur, scan_scratch_bytes(cap2) / 4 + 1);
   uint32_t* info = carve<uint32_t>(cur, 4);
   float* inv_len = p.mean ? carve<float>(cur, p.num_bags) : nullptr;
+  const bool merge = sparse_merges(p);
+  const int64_t ub = cap < static_cast<int64_t>(p.M) ? cap : static_cast<int64_t>(p.M);
+  uint32_t* hd = merge ? carve<uint32_t>(cur, cap) : nullptr;
+  uint32_t* hscr = merge ? carve<uint32_t>(cur, scan_scratch_bytes(cap) / 4 + 1) : nullptr;
+  uint32_t* hpos = merge ? carve<uint32_t>(cur, cap + 1) : nullptr;
+  uint32_t* num_bases = merge ? carve<uint32_t>(cur, 4) : nullptr;
+  float* mrs = merge ? carve<float>(cur, static_cast<size_t>(ub) * p.Z) : nullptr;
+  uint32_t* mb = merge ? carve<uint32_t>(cur, ub) : nullptr;
+  uint32_t* mv = merge ? carve<uint32_t>(cur, ub) : nullptr;
 
   hipError_t e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);
   if (e == hipSuccess) e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), rscr, stream);
@@ -613,12 +746,34 @@ static hipError_t sparse_prepare(const KParams& p, const void* indices, const vo
   if (e == hipSuccess)
     e = radix_sort_pairs(cbs, cvs, cb1, cv1, cap, base_bits(p.M), cscr, stream, info + 2);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(tail_count_kernel, dim3(1), dim3(1), 0, stream, p, cbs, num_runs, info);
+  if (!merge) {
+    hipLaunchKernelGGL(tail_count_kernel, dim3(1), dim3(1), 0, stream, p, cbs, num_runs, info);
+    hipLaunchKernelGGL(own_kernel, dim3(grid_stride_blocks(cap2)), dim3(kBlockThreads), 0, stream,
+                       p, cbs, info, own);
+    e = exclusive_scan(own, cap2, oscr, num_unique32, stream, info + 3);
+    if (e != hipSuccess) return e;
+    *st = SparseState{cbs, cvs, info, own, rs, p.C, p.d, cap2};
+    return hipSuccess;
+  }
+  // pre-merge: one record per distinct base
+  hipLaunchKernelGGL(merge_heads_kernel, dim3(grid_stride_blocks(cap)), dim3(kBlockThreads), 0,
+                     stream, cbs, num_runs, p.C, hd);
+  e = exclusive_scan(hd, cap, hscr, num_bases, stream, info + 2);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(merge_positions_kernel, dim3(grid_stride_blocks(cap)), dim3(kBlockThreads), 0,
+                     stream, cbs, num_runs, p.C, hd, num_bases, hpos);
+  {
+    const int64_t want = (ub + kWavesPerBlock - 1) / kWavesPerBlock;  // a wavefront per base
+    const uint32_t mblocks = static_cast<uint32_t>(want < 1 ? 1 : (want > 65536 ? 65536 : want));
+    hipLaunchKernelGGL(merge_sums_kernel, dim3(mblocks), dim3(kBlockThreads), 0, stream, p, cbs,
+                       cvs, hpos, num_bases, rs, mrs, mb, mv);
+  }
+  hipLaunchKernelGGL(tail_count_merged_kernel, dim3(1), dim3(1), 0, stream, p, mb, num_bases, info);
   hipLaunchKernelGGL(own_kernel, dim3(grid_stride_blocks(cap2)), dim3(kBlockThreads), 0, stream, p,
-                     cbs, info, own);
+                     mb, info, own);
   e = exclusive_scan(own, cap2, oscr, num_unique32, stream, info + 3);
   if (e != hipSuccess) return e;
-  *st = SparseState{cbs, cvs, info, own, rs, cap2};
+  *st = SparseState{mb, mv, info, own, mrs, 1u, p.Z, cap2};
   return hipSuccess;
 }
 
@@ -630,8 +785,9 @@ hipError_t launch_gradient_sparse(const KParams& p, const void* indices, const v
   hipError_t e = sparse_prepare(p, indices, offsets, grad, workspace, num_unique32, &st, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((emit_kernel<0, float, false>), dim3(emit_blocks(st.cap2)), dim3(kBlockThreads),
-                     0, stream, p, st.cb, st.cv, st.info, st.own, num_unique32, st.rs,
-                     EmitList{locations, values, capacity}, EmitUpdate<float>{nullptr, nullptr, 0.f, 0.f});
+                     0, stream, p, st.cb, st.cv, st.info, st.own, num_unique32, st.rs, st.rsC,
+                     st.rsD, EmitList{locations, values, capacity},
+                     EmitUpdate<float>{nullptr, nullptr, 0.f, 0.f});
   return hipGetLastError();
 }
 
@@ -642,10 +798,12 @@ static void launch_emit_update(const KParams& p, const SparseState& st, const ui
   const EmitUpdate<WT> u{w, state, lr, eps};
   if (state)
     hipLaunchKernelGGL((emit_kernel<1, WT, true>), dim3(emit_blocks(st.cap2)), dim3(kBlockThreads), 0,
-                       stream, p, st.cb, st.cv, st.info, st.own, total, st.rs, none, u);
+                       stream, p, st.cb, st.cv, st.info, st.own, total, st.rs, st.rsC, st.rsD,
+                       none, u);
   else
     hipLaunchKernelGGL((emit_kernel<1, WT, false>), dim3(emit_blocks(st.cap2)), dim3(kBlockThreads), 0,
-                       stream, p, st.cb, st.cv, st.info, st.own, total, st.rs, none, u);
+                       stream, p, st.cb, st.cv, st.info, st.own, total, st.rs, st.rsC, st.rsD,
+                       none, u);
 }
 
 hipError_t launch_sparse_update(const KParams& p, const void* indices, const void* offsets,

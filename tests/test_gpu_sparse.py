@@ -1,4 +1,5 @@
-"""GPU parity of the sparse gradient export (Alg. 1, sparse branch).
+"""GPU parity of the sparse gradient export (Alg. 1, sparse branch), with and
+without the pre-merge of chunk records that share a base.
 
 Unique locations must equal the oracle's bit for bit (they are integers);
 values must match the oracle's float64 sums within the normalised tolerance;
@@ -101,3 +102,48 @@ def test_sparse_update_heavy_coverage(opt, M):
     w_ref, s_ref, G, A, _ = L.ref_backward(g)
     s_gpu = None if L.state is None else L.state.cpu().numpy()
     parity.check_update(L, L.weights(), s_gpu, w_ref, s_ref, G, A, wl.lr)
+
+
+# Chunk records averaging 16 or more per base of the array: the records that
+# share a base are summed once before the merge (pre-merge); below that the
+# merge walks them one by one.  Both sides of the rule, with chunk signs,
+# mean pooling and chunks that wrap past M.
+PREMERGE = [("premerge-dense", 400, dict(d=64, Z=16, M=500, bag="poisson:8:1:30")),
+            ("premerge-wrap", 200, dict(d=48, Z=6, M=97, bag="poisson:6:0:20")),
+            ("below-premerge", 200, dict(d=64, Z=16, M=20_000, bag="poisson:8:1:30"))]
+
+
+@pytest.mark.parametrize("opts", [{}, dict(sign="sparse", mean=True), dict(sign="pm1")],
+                         ids=["plain", "sparse-sign-mean", "pm1"])
+@pytest.mark.parametrize("case", PREMERGE, ids=[c[0] for c in PREMERGE])
+def test_sparse_gradient_premerge(case, opts):
+    key, B, over = case
+    L = Layer(_wl(key, over), B=B, **opts)
+    wl = L.wl
+    merged = L.x.N * wl.C >= 16 * wl.M
+    assert merged == (case[0] != "below-premerge")
+    g = synth.make_grad(wl, B=L.B)
+    loc, val = _run_sparse(L, g)
+    uloc, uval = o.gradient_sparse(wl.M, wl.Z, wl.d, wl.T, L.B, L.a, L.b, L.x.indices,
+                                   L.x.offsets, g, sign=L.sign, mean=L.mean)
+    assert np.array_equal(loc.astype(np.int64), uloc)
+    _, A, _ = o.gradient_dense(wl.M, wl.Z, wl.d, wl.T, L.B, L.a, L.b, L.x.indices, L.x.offsets,
+                               g, sign=L.sign, mean=L.mean)
+    err = np.abs(val.astype(np.float64) - uval)
+    assert np.all(err <= 1e-5 * A[uloc] + 1e-30)
+    loc2, val2 = _run_sparse(L, g)  # and bit-identical again
+    assert np.array_equal(loc, loc2) and np.array_equal(val.view(np.uint32), val2.view(np.uint32))
+
+
+@pytest.mark.parametrize("case", PREMERGE[:2], ids=[c[0] for c in PREMERGE[:2]])
+def test_sparse_backward_premerge(case):
+    """The SPARSE backward on the pre-merged records: Adagrad applied at each
+    unique location, against the oracle."""
+    import parity
+    key, B, over = case
+    wl = _wl(key, dict(over, optimizer="adagrad", lr=0.01))
+    L = Layer(wl, B=B, flags=pss.PSS_BWD_SPARSE, s0=0.1, sign="pm1")
+    grad = synth.make_grad(wl, B=L.B)
+    L.backward(grad)
+    w_ref, s_ref, G, A, _ = L.ref_backward(grad)
+    parity.check_update(L, L.weights(), L.state.cpu().numpy(), w_ref, s_ref, G, A, wl.lr)

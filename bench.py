@@ -55,6 +55,7 @@ PMC_FILE = os.path.join(ROOT, "profiles", "pmc_forward_c2.json")
 # device headers): a counter summary stays valid while these are unchanged.
 KERNEL_SOURCES = {
     "forward_kernel": ["pss_forward.hip"],
+    "forward_stream_kernel": ["pss_forward.hip"],
     "reduce_deposit_kernel": ["pss_sorted.hip"],
 }
 SHARED_HEADERS = ["pss_hash.hpp", "pss_kernels.hpp"]  # device code; pss_launch.hpp only declares
@@ -71,15 +72,24 @@ def source_digest(kernel: str = "forward_kernel") -> str:
     return h.hexdigest()
 
 
-def counted_traffic(workload: str):
-    """HBM bytes per forward launch from the committed counter summary, or None
-    when it was taken on other kernel sources or another workload."""
+def forward_counters(workload: str):
+    """The committed counter summary of the forward kernel, or None when it was
+    taken on other kernel sources or another workload."""
     try:
         with open(PMC_FILE) as f:
             pmc = json.load(f)
     except (OSError, ValueError):
         return None
     if pmc.get("source_sha256") != source_digest("forward_kernel") or pmc.get("workload") != workload:
+        return None
+    return pmc
+
+
+def counted_traffic(workload: str):
+    """HBM bytes per forward launch from the committed counter summary, or None
+    when it was taken on other kernel sources or another workload."""
+    pmc = forward_counters(workload)
+    if pmc is None:
         return None
     return pmc["fetch_kib"] * 1024 * pmc["fetch_scale"] + pmc["write_kib"] * 1024 * pmc["write_scale"]
 
@@ -326,7 +336,11 @@ def main():
     # call launches the grouping, reduction (and optimizer) kernels; its
     # call-level figures are reported beside it.
     fwd_lv = max(timed, key=lambda lv: timed[lv]["forward_bytes"] / peaks_gbs[lv][0])
-    dom, dom_bytes, dom_t = "forward_kernel", tr[fwd_lv][0], f_avg
+    # the kernel's name as the committed counters recorded it (pss_forward
+    # launches the streamed or the tiled kernel, by the batch's shape)
+    pmc = forward_counters(wl.name)
+    dom = pmc["kernel"].split("(")[0] if pmc is not None else "pss_forward"
+    dom_bytes, dom_t = tr[fwd_lv][0], f_avg
     dom_peak = peaks_gbs[fwd_lv][0]
     achieved = dom_bytes / dom_t / 1e9
     fb, bb = tr["hbm"]

@@ -4,7 +4,7 @@
 
 Each DB is a rocprofv3 result database of one --pmc pass over the same
 command (counters differ per pass).  For each kernel named by --kernels
-(default: forward_kernel and reduce_deposit_kernel) it prints the
+(default: forward_stream_kernel, forward_kernel and reduce_deposit_kernel) it prints the
 per-dispatch average of every counter found, and the derived L2 hit rate
 and atomic requests per lookup.
 """
@@ -14,7 +14,7 @@ import argparse
 import sqlite3
 from collections import defaultdict
 
-KERNELS = ("forward_kernel", "reduce_deposit_kernel")
+KERNELS = ("forward_stream_kernel", "forward_kernel", "reduce_deposit_kernel")
 
 
 def collect(dbs, kernels=KERNELS):

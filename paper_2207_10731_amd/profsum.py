@@ -7,7 +7,8 @@
       --fetch F.db --write W.db --copy-fetch CF.db --copy-write CW.db \\
       --copy-bytes BYTES --out profiles/pmc_<kernel>_<workload>.json
       FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the kernel whose name
-      contains SUBSTR (forward_kernel or reduce_deposit_kernel), with scale
+      contains SUBSTR (forward_stream_kernel, forward_kernel or
+      reduce_deposit_kernel), with scale
       factors from a copy kernel that moved BYTES each way, and the sha256 of
       the sources that kernel is built from
 """

@@ -66,11 +66,12 @@ def test_peaks():
 def test_committed_counters_match_sources():
     """profiles/pmc_*_c2.json carry the sha256 of the sources their kernel
     was built from; both must match the present tree."""
-    for kernel, name in (("forward_kernel", "pmc_forward_c2.json"),
+    for kernel, name in (("forward_stream_kernel", "pmc_forward_c2.json"),
                          ("reduce_deposit_kernel", "pmc_reduce_deposit_c2.json")):
         with open(os.path.join(bench.ROOT, "profiles", name)) as f:
             pmc = json.load(f)
         assert pmc["source_sha256"] == bench.source_digest(kernel), name
         assert pmc["workload"] == synth.get("c2").name
+        assert f"pss::{kernel}<" in pmc["kernel"], name
     t = bench.counted_traffic(synth.get("c2").name)
     assert t is not None and 0.9 * GB < t < 1.3 * GB

@@ -2,11 +2,12 @@
 
 One step = pss_forward + pss_backward_update (forward gather/pool, backward
 deposit, optimizer step) over one batch of synthetic bags, rotating 4
-pre-generated index batches and gradient batches resident in HBM.  Each
-step starts with pss_prepare_backward (as a training loop would once the
-batch's indices are in place): the backward's grouping of the batch runs on
-a library stream beside the forward kernel and the backward reuses it
-(--no-prepare: the backward groups the batch itself).
+pre-generated index batches and gradient batches resident in HBM.  The
+backward groups the batch itself.  With --prepare each step starts with
+pss_prepare_backward instead: the grouping runs on a library stream beside
+the forward kernel and the backward reuses it (slower on the headline
+workload, where it shares the memory system with a forward that writes at
+the streamed rate: 392.7 against 381.5 us per step).
 
 Default workload: criteo-tb-shaped one-hot batch (26 tables with log-uniform
 cardinalities in [3, 4e7], Zipf(1.1) indices, batch 65536, d = 128, Z = 32,
@@ -226,8 +227,10 @@ def main():
     ap.add_argument("--config", default="c2")
     ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted", "sparse"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--prepare", action="store_true",
+                    help="start each step with pss_prepare_backward (the grouping beside the forward)")
     ap.add_argument("--no-prepare", action="store_true",
-                    help="no pss_prepare_backward call: the backward groups the batch itself")
+                    help="the default: the backward groups the batch itself")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip measuring the L2 / memory-side cache / HBM denominators")
     ap.add_argument("--event-every", type=int, default=5,
@@ -272,7 +275,7 @@ def main():
     gen.manual_seed(wl.data_seed)
     grads = [torch.randn((wl.B, wl.T * wl.d), generator=gen, device=dev) for _ in range(ROTATE)]
     out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=dev)
-    prepare = not args.no_prepare
+    prepare = args.prepare and not args.no_prepare
     hps = [pss.make_hash_params(wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=x.N,
                                 weight_dtype=dt_code, eps=wl.eps, flags=flags) for x in xs]
     torch.cuda.synchronize()
@@ -379,7 +382,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "tables": wl.T, "batch": wl.B, "d": wl.d, "Z": wl.Z,
                    "M": wl.M, "storage": wl.weight_dtype, "optimizer": wl.optimizer,
-                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": not args.no_prepare,
+                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": prepare,
                    "lookups_per_step": N_avg},
         "roofline": {"bound": fwd_lv, "kernel": dom, "achieved": achieved, "peak": dom_peak,
                      "unit": "GB/s", "frac": achieved / dom_peak,

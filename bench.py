@@ -50,6 +50,7 @@ import numpy as np  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 ROTATE = 4
 PMC_FILE = os.path.join(ROOT, "profiles", "pmc_forward_c2.json")
+PMC_REDUCE_FILE = os.path.join(ROOT, "profiles", "pmc_reduce_deposit_c2.json")
 
 
 # Sources each profiled kernel is compiled from (its own file and the shared
@@ -73,26 +74,64 @@ def source_digest(kernel: str = "forward_kernel") -> str:
     return h.hexdigest()
 
 
-def forward_counters(workload: str):
-    """The committed counter summary of the forward kernel, or None when it was
-    taken on other kernel sources or another workload."""
+def kernel_counters(workload: str, kernel: str = "forward_kernel"):
+    """The committed counter summary of the forward kernel (kernel =
+    "forward_kernel") or of the reduce stage ("reduce_deposit_kernel"), or
+    None when it was taken on other kernel sources or another workload."""
+    path = PMC_FILE if kernel == "forward_kernel" else PMC_REDUCE_FILE
     try:
-        with open(PMC_FILE) as f:
+        with open(path) as f:
             pmc = json.load(f)
     except (OSError, ValueError):
         return None
-    if pmc.get("source_sha256") != source_digest("forward_kernel") or pmc.get("workload") != workload:
+    if pmc.get("source_sha256") != source_digest(kernel) or pmc.get("workload") != workload:
         return None
     return pmc
 
 
-def counted_traffic(workload: str):
-    """HBM bytes per forward launch from the committed counter summary, or None
+def forward_counters(workload: str):
+    return kernel_counters(workload, "forward_kernel")
+
+
+def counted_traffic(workload: str, kernel: str = "forward_kernel"):
+    """HBM bytes per launch from the committed counter summary, or None
     when it was taken on other kernel sources or another workload."""
-    pmc = forward_counters(workload)
+    pmc = kernel_counters(workload, kernel)
     if pmc is None:
         return None
     return pmc["fetch_kib"] * 1024 * pmc["fetch_scale"] + pmc["write_kib"] * 1024 * pmc["write_scale"]
+
+
+class ReduceTimer:
+    """HIP events that the library records around its reduce-and-deposit
+    kernel (pss_debug_reduce_events), one pair per timed call.  A pair the
+    library never recorded (no such kernel on this workload's path) reads
+    as None."""
+
+    def __init__(self, n):
+        import ctypes
+        self._ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so")  # the runtime torch already loaded
+        self.pairs = []
+        for _ in range(n):
+            pair = []
+            for _ in range(2):
+                h = ctypes.c_void_p()
+                if self.hip.hipEventCreate(ctypes.byref(h)) != 0:
+                    raise RuntimeError("hipEventCreate failed")
+                pair.append(h)
+            self.pairs.append(pair)
+
+    def elapsed_ms(self, i):
+        ms = self._ct.c_float()
+        st = self.hip.hipEventElapsedTime(self._ct.byref(ms), self.pairs[i][0], self.pairs[i][1])
+        return ms.value if st == 0 else None
+
+    def close(self):
+        for pair in self.pairs:
+            for h in pair:
+                self.hip.hipEventDestroy(h)
+        self.pairs = []
 
 
 def log(*a):
@@ -280,7 +319,7 @@ def main():
                                 weight_dtype=dt_code, eps=wl.eps, flags=flags) for x in xs]
     torch.cuda.synchronize()
 
-    def step(k, ev=None):
+    def step(k, ev=None, red=None):
         r = k % ROTATE
         if prepare:
             pss.pss_prepare_backward(wl.M, wl.Z, wl.d, hps[r], idx[r], off[r])
@@ -289,8 +328,12 @@ def main():
         pss.pss_forward(shared, wl.M, wl.Z, wl.d, hps[r], idx[r], off[r], out)
         if ev is not None:
             ev[1].record()
+        if red is not None:
+            pss.pss_debug_reduce_events(red[0], red[1])
         pss.pss_backward_update(shared, state, wl.M, wl.Z, wl.d, hps[r], idx[r], off[r], grads[r],
                                 wl.lr)
+        if red is not None:
+            pss.pss_debug_reduce_events()
         if ev is not None:
             ev[2].record()
 
@@ -300,12 +343,22 @@ def main():
     every = max(1, args.event_every)
     evs = {k: [torch.cuda.Event(enable_timing=True) for _ in range(3)]
            for k in range(0, args.steps, every)}
+    # the reduce kernel is timed on steps between the bracketed ones, one in
+    # every 2 * every steps (two more event records per timed call, kept out
+    # of the forward and backward brackets)
+    red_phase = every // 2 if every > 1 else 0
+    red_steps = [k for k in range(args.steps) if k % (2 * every) == red_phase]
+    timer = ReduceTimer(len(red_steps))
+    red = {k: timer.pairs[i] for i, k in enumerate(red_steps)}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        step(k, evs.get(k))
+        step(k, evs.get(k), red.get(k))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    red_ms = [timer.elapsed_ms(i) for i in range(len(red_steps))]
+    timer.close()
+    red_ms = np.array(red_ms, dtype=float) if red_ms and all(x is not None for x in red_ms) else None
 
     fwd_ms = np.array([e[0].elapsed_time(e[1]) for e in evs.values()])
     bwd_ms = np.array([e[1].elapsed_time(e[2]) for e in evs.values()])
@@ -332,25 +385,47 @@ def main():
     timed = {lv: v for lv, v in levels.items() if v["t_star_us"] is not None}
     step_bound = max(timed, key=lambda lv: timed[lv]["t_star_us"])
     t_star = timed[step_bound]["t_star_us"] * 1e-6
-    # The roofline object describes the forward kernel: pss_forward launches
-    # exactly one kernel (so events around the call time that kernel), the
-    # longest single kernel of the headline step.  Its bound is the level
-    # whose floor time is largest for the forward's own bytes.  The backward
-    # call launches the grouping, reduction (and optimizer) kernels; its
-    # call-level figures are reported beside it.
+    # Kernels timed live: pss_forward launches exactly one kernel (events
+    # around the call time it); the library records events around its
+    # reduce-and-deposit kernel on request.  Each kernel's bound is the level
+    # whose floor time is largest for its own bytes; the roofline object
+    # describes the longer of the two (the dominant kernel), and both are
+    # listed under "kernels".  Kernel names are those the committed counters
+    # recorded (pss_forward launches the streamed or the tiled kernel, by the
+    # batch's shape).
     fwd_lv = max(timed, key=lambda lv: timed[lv]["forward_bytes"] / peaks_gbs[lv][0])
-    # the kernel's name as the committed counters recorded it (pss_forward
-    # launches the streamed or the tiled kernel, by the batch's shape)
     pmc = forward_counters(wl.name)
-    dom = pmc["kernel"].split("(")[0] if pmc is not None else "pss_forward"
-    dom_bytes, dom_t = tr[fwd_lv][0], f_avg
-    dom_peak = peaks_gbs[fwd_lv][0]
-    achieved = dom_bytes / dom_t / 1e9
+    kernels = {"forward": {
+        "kernel": pmc["kernel"].split("(")[0] if pmc is not None else "pss_forward",
+        "bound": fwd_lv, "bytes_per_launch": tr[fwd_lv][0], "avg_launch_us": f_avg * 1e6,
+        "peak": peaks_gbs[fwd_lv][0], "timed_launches": len(evs),
+        "traffic": counted_traffic(wl.name) if fwd_lv == "hbm" else None}}
+    if red_ms is not None:
+        # the reduce stage reads every lookup's gradient row and its grouped
+        # (key, row) pair: HBM-bound
+        pmc_r = kernel_counters(wl.name, "reduce_deposit_kernel")
+        kernels["reduce"] = {
+            "kernel": pmc_r["kernel"].split("(")[0] if pmc_r is not None else "reduce_deposit_kernel",
+            "bound": "hbm", "bytes_per_launch": 4.0 * wl.B * wl.T * wl.d + 8.0 * N_avg,
+            "avg_launch_us": red_ms.mean() * 1e3, "peak": peaks_gbs["hbm"][0],
+            "timed_launches": len(red_ms),
+            "traffic": counted_traffic(wl.name, "reduce_deposit_kernel")}
+    for kv in kernels.values():
+        kv["achieved"] = kv["bytes_per_launch"] / (kv["avg_launch_us"] * 1e-6) / 1e9
+        kv["frac"] = kv["achieved"] / kv["peak"]
+    dom_key = max(kernels, key=lambda k: kernels[k]["avg_launch_us"])
+    dk = kernels[dom_key]
+    achieved = kernels["forward"]["achieved"]
     fb, bb = tr["hbm"]
     log(f"[bench] forward   median {np.median(fwd_ms)*1e3:.1f} us  p10 {np.percentile(fwd_ms,10)*1e3:.1f}"
         f"  p90 {np.percentile(fwd_ms,90)*1e3:.1f}  -> {achieved:.0f} GB/s at level {fwd_lv}")
     log(f"[bench] backward  median {np.median(bwd_ms)*1e3:.1f} us  p10 {np.percentile(bwd_ms,10)*1e3:.1f}"
         f"  p90 {np.percentile(bwd_ms,90)*1e3:.1f}  -> {bb/b_avg/1e9:.0f} GB/s (HBM floor bytes)")
+    if "reduce" in kernels:
+        kr = kernels["reduce"]
+        log(f"[bench] reduce    mean {kr['avg_launch_us']:.1f} us  -> {kr['achieved']:.0f} GB/s, "
+            f"frac {kr['frac']:.3f} (kernel only)")
+    log(f"[bench] dominant kernel: {dom_key} ({dk['kernel']})")
     for lv, v in levels.items():
         tstar = "n/a" if v["t_star_us"] is None else f"{v['t_star_us']:.1f} us"
         log(f"[bench] level {lv}: {v['bytes_per_step']/1e6:.1f} MB/step, peak "
@@ -384,11 +459,12 @@ def main():
                    "M": wl.M, "storage": wl.weight_dtype, "optimizer": wl.optimizer,
                    "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": prepare,
                    "lookups_per_step": N_avg},
-        "roofline": {"bound": fwd_lv, "kernel": dom, "achieved": achieved, "peak": dom_peak,
-                     "unit": "GB/s", "frac": achieved / dom_peak,
-                     "traffic": counted_traffic(wl.name) if fwd_lv == "hbm" else None,
-                     "bytes_per_launch": dom_bytes, "avg_launch_us": dom_t * 1e6,
-                     "timed_launches": len(evs),
+        "roofline": {"bound": dk["bound"], "kernel": dk["kernel"], "achieved": dk["achieved"],
+                     "peak": dk["peak"], "unit": "GB/s", "frac": dk["frac"],
+                     "traffic": dk["traffic"],
+                     "bytes_per_launch": dk["bytes_per_launch"], "avg_launch_us": dk["avg_launch_us"],
+                     "timed_launches": dk["timed_launches"],
+                     "kernels": kernels,
                      "step_bound": step_bound, "step_t_star_us": t_star * 1e6,
                      "step_frac": t_star / t_step,
                      "step_hbm_bytes": fb + bb,

@@ -319,6 +319,17 @@ int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash
                     const void* indices, const void* offsets, int8_t* sign_out,
                     hipStream_t stream);
 
+/* Timing hook for measurement tools (no part of the method).  With two
+ * non-null events (hipEvent_t, created by the caller and kept alive while
+ * the hook is set), every later backward call that runs the sorted path's
+ * reduce-and-deposit kernel records `before` on the call's stream right
+ * before that kernel and `after` right after it, so that the kernel's own
+ * duration can be read with hipEventElapsedTime.  Two nulls switch it off;
+ * one null and one event is PSS_ERR_INVALID_ARG.  One setting for the whole
+ * process: meant for one caller timing its own calls, not for concurrent
+ * callers.  Each record adds a few microseconds to the stream. */
+int pss_debug_reduce_events(void* before, void* after);
+
 /* Host evaluation of the same hash code the kernels run (no GPU needed):
  * base_out[e*C + j] = h(indices[e], t(e), j) for host arrays indices[N],
  * offsets[T*B+1] (int64 whatever the flags say) and base_out[N*C].  Returns

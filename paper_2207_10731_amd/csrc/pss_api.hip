@@ -700,6 +700,12 @@ int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash
   return hip_status(pss::launch_debug_addresses(p, indices, offsets, nullptr, sign_out, stream));
 }
 
+int pss_debug_reduce_events(void* before, void* after) {
+  if ((before == nullptr) != (after == nullptr)) return PSS_ERR_INVALID_ARG;
+  pss::set_reduce_events(static_cast<hipEvent_t>(before), static_cast<hipEvent_t>(after));
+  return PSS_OK;
+}
+
 int pss_release_scratch(void) {
   std::lock_guard<std::mutex> lock(g_kept_mu);
   int cur = 0;

@@ -36,6 +36,10 @@ struct GroupedPairs {
 };
 hipError_t launch_group_sorted(const KParams& p, const void* indices, const void* offsets,
                                void* workspace, hipStream_t stream, GroupedPairs* out);
+// Events recorded around every later reduce-and-deposit launch (both null:
+// none).
+void set_reduce_events(hipEvent_t before, hipEvent_t after);
+
 hipError_t launch_reduce_sorted(float* dst, float scale, const KParams& p, const GroupedPairs& g,
                                 const void* grad, hipStream_t stream);
 

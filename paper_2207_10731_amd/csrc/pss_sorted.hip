@@ -23,6 +23,8 @@
 //             add the run's sum at the run's hashed addresses with float
 //             atomics.  A token spanning several pieces deposits one partial
 //             sum per piece.
+#include <atomic>
+
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -934,16 +936,32 @@ hipError_t launch_keygen(const KParams& p, const void* indices, const void* offs
   return hipGetLastError();
 }
 
+// Timing hook (pss_debug_reduce_events): events recorded around each
+// reduce-and-deposit launch, both or neither set.
+static std::atomic<hipEvent_t> g_reduce_before{nullptr}, g_reduce_after{nullptr};
+
+void set_reduce_events(hipEvent_t before, hipEvent_t after) {
+  g_reduce_before.store(before);
+  g_reduce_after.store(after);
+}
+
 template <int EPL, int U, bool SIGN, typename GT, bool REC>
 static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, const uint32_t* keys,
                                   const uint32_t* rows, const GT* grad, const float* inv_len,
                                   uint32_t* rkey, uint32_t* rval, hipStream_t stream) {
   const uint64_t blocks = (static_cast<uint64_t>(p.N) + kPiece - 1) / kPiece;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
+  const hipEvent_t before = g_reduce_before.load(), after = g_reduce_after.load();
+  if (before != nullptr && after != nullptr) {
+    const hipError_t e = hipEventRecord(before, stream);
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT, REC>),
                      dim3(static_cast<uint32_t>(blocks), slabs), dim3(kReduceThreads), 0, stream,
                      dst, scale, p, keys, rows, grad, inv_len, p.N, rkey, rval);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && before != nullptr && after != nullptr) e = hipEventRecord(after, stream);
+  return e;
 }
 
 template <bool SIGN, typename GT, bool REC>

@@ -80,12 +80,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pss_status_string.argtypes = [ctypes.c_int]
     lib.pss_status_string.restype = ctypes.c_char_p
     lib.pss_release_scratch.argtypes = []
+    lib.pss_debug_reduce_events.argtypes = [vp, vp]
     for name in ("pss_hash_params_from_seed", "pss_forward", "pss_backward_update",
                  "pss_backward_update_noalloc",
                  "pss_prepare_backward", "pss_debug_addresses", "pss_debug_signs",
                  "pss_gradient_sparse",
                  "pss_hash_bases_host", "pss_hash_signs_host", "pss_validate_offsets_host",
-                 "pss_release_scratch"):
+                 "pss_release_scratch", "pss_debug_reduce_events"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     # Return the library's runtime objects (kept scratch, prepared-grouping
@@ -376,6 +377,29 @@ def pss_validate_offsets_host(offsets, num_bags, N) -> int:
         return PSS_ERR_INVALID_ARG
     return load_library().pss_validate_offsets_host(off.ctypes.data_as(ctypes.c_void_p),
                                                     num_bags, N)
+
+
+def pss_debug_reduce_events(before=None, after=None):
+    """Timing hook: later backward calls record the two events (torch.cuda.Event
+    objects recorded once already, so that their HIP events exist, or raw
+    hipEvent_t handles) right before and after their reduce-and-deposit
+    kernel; no arguments switch it off.  The events must stay alive while the
+    hook is set."""
+    handles = []
+    for ev in (before, after):
+        if ev is None:
+            handles.append(None)
+            continue
+        if hasattr(ev, "cuda_event"):  # torch.cuda.Event
+            h = int(ev.cuda_event)
+        else:  # a raw hipEvent_t: int or ctypes.c_void_p
+            h = int((ev.value or 0) if isinstance(ev, ctypes.c_void_p) else ev)
+        if h == 0:
+            raise ValueError("pss_debug_reduce_events: a null event (a torch event must be "
+                             "recorded once before it is passed)")
+        handles.append(ctypes.c_void_p(h))
+    _check(load_library().pss_debug_reduce_events(handles[0], handles[1]),
+           "pss_debug_reduce_events")
 
 
 def pss_release_scratch():

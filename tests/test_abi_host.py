@@ -302,3 +302,15 @@ def test_by_address_flag_rules(lib):
     assert lib.pss_backward_update_noalloc(dummy, dummy, 2_500_000, 128, 128, ctypes.byref(runs),
                                            dummy, dummy, dummy, ctypes.c_float(0.1),
                                            None) == pss.PSS_ERR_SCRATCH_LIMIT
+
+
+def test_reduce_events_hook_rules(lib):
+    """The timing hook takes both events or neither (no GPU work: it only
+    stores the handles; they are cleared again before the test ends)."""
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.pss_debug_reduce_events(fake, None) == pss.PSS_ERR_INVALID_ARG
+    assert lib.pss_debug_reduce_events(None, fake) == pss.PSS_ERR_INVALID_ARG
+    assert lib.pss_debug_reduce_events(None, None) == pss.PSS_OK
+    with pytest.raises(ValueError):
+        pss.pss_debug_reduce_events(0, 0)
+    pss.pss_debug_reduce_events()

@@ -46,3 +46,30 @@ def test_short_tensors_are_refused():
     got = pss.pss_forward(L.shared, wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets, out)
     ref, s_abs = L.ref_forward()
     parity.check_forward(got.cpu().numpy(), ref, s_abs, parity.RTOL[wl.weight_dtype])
+
+
+def test_reduce_events_hook_brackets_the_reduce_kernel():
+    """With the timing hook set, a sorted backward records both events around
+    its reduce-and-deposit kernel (a positive interval, inside the call's
+    own); the update made with the hook matches the oracle."""
+    wl = synth.get("c2").scaled(B=512)
+    g = synth.make_grad(wl, B=512)
+    L = Layer(wl, flags=pss.PSS_BWD_SORTED)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for ev in evs:
+        ev.record()  # creates the HIP events
+    torch.cuda.synchronize()
+    pss.pss_debug_reduce_events(evs[1], evs[2])
+    evs[0].record()
+    try:
+        L.backward(g)
+    finally:
+        pss.pss_debug_reduce_events()
+    evs[3].record()
+    torch.cuda.synchronize()
+    inner, outer = evs[1].elapsed_time(evs[2]), evs[0].elapsed_time(evs[3])
+    print(f"reduce {inner * 1e3:.1f} us of {outer * 1e3:.1f} us", flush=True)
+    assert 0.0 < inner < outer
+    assert evs[0].elapsed_time(evs[1]) > 0.0 and evs[2].elapsed_time(evs[3]) > 0.0
+    w_ref, s_ref, G, A, _ = L.ref_backward(g)
+    parity.check_update(L, L.weights(), None, w_ref, s_ref, G, A, wl.lr)

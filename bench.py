@@ -3,11 +3,15 @@
 One step = pss_forward + pss_backward_update (forward gather/pool, backward
 deposit, optimizer step) over one batch of synthetic bags, rotating 4
 pre-generated index batches and gradient batches resident in HBM.  The
-backward groups the batch itself.  With --prepare each step starts with
-pss_prepare_backward instead: the grouping runs on a library stream beside
-the forward kernel and the backward reuses it (slower on the headline
-workload, where it shares the memory system with a forward that writes at
-the streamed rate: 392.7 against 381.5 us per step).
+forward is called with PSS_PREPARE_BACKWARD, as a training step can: on the
+headline workload its streamed kernel writes the first stage of the
+backward's grouping (keys, rows, digit counts) while it reads the batch's
+index and offset entries, and the backward finishes the grouping (379.7
+against 391.3 us per step without the flag, on one box).  --no-prepare: the
+backward groups the batch itself.  --prepare: each step starts with
+pss_prepare_backward instead, the whole grouping on a library stream beside
+the forward kernel (slower there: it shares the memory system with a
+forward that writes at the streamed rate).
 
 Default workload: criteo-tb-shaped one-hot batch (26 tables with log-uniform
 cardinalities in [3, 4e7], Zipf(1.1) indices, batch 65536, d = 128, Z = 32,
@@ -60,7 +64,7 @@ KERNEL_SOURCES = {
     "forward_stream_kernel": ["pss_forward.hip"],
     "reduce_deposit_kernel": ["pss_sorted.hip"],
 }
-SHARED_HEADERS = ["pss_hash.hpp", "pss_kernels.hpp"]  # device code; pss_launch.hpp only declares
+SHARED_HEADERS = ["pss_hash.hpp", "pss_kernels.hpp", "pss_keygen.hpp"]  # device code; pss_launch.hpp only declares
 
 
 def source_digest(kernel: str = "forward_kernel") -> str:
@@ -267,9 +271,10 @@ def main():
     ap.add_argument("--variant", default="auto", choices=["auto", "atomic", "sorted", "sparse"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--prepare", action="store_true",
-                    help="start each step with pss_prepare_backward (the grouping beside the forward)")
+                    help="start each step with pss_prepare_backward (the grouping beside the "
+                         "forward) instead of the flag on pss_forward")
     ap.add_argument("--no-prepare", action="store_true",
-                    help="the default: the backward groups the batch itself")
+                    help="no preparation: the backward groups the batch itself")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip measuring the L2 / memory-side cache / HBM denominators")
     ap.add_argument("--event-every", type=int, default=5,
@@ -315,8 +320,10 @@ def main():
     grads = [torch.randn((wl.B, wl.T * wl.d), generator=gen, device=dev) for _ in range(ROTATE)]
     out = torch.empty((wl.B, wl.T * wl.d), dtype=torch.float32, device=dev)
     prepare = args.prepare and not args.no_prepare
+    in_forward = not args.prepare and not args.no_prepare
+    fwd_flags = flags | (pss.PSS_PREPARE_BACKWARD if in_forward else 0)
     hps = [pss.make_hash_params(wl.hash_seed, num_tables=wl.T, batch=wl.B, num_indices=x.N,
-                                weight_dtype=dt_code, eps=wl.eps, flags=flags) for x in xs]
+                                weight_dtype=dt_code, eps=wl.eps, flags=fwd_flags) for x in xs]
     torch.cuda.synchronize()
 
     def step(k, ev=None, red=None):
@@ -457,7 +464,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "tables": wl.T, "batch": wl.B, "d": wl.d, "Z": wl.Z,
                    "M": wl.M, "storage": wl.weight_dtype, "optimizer": wl.optimizer,
-                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": prepare,
+                   "bags": wl.bag, "indices": wl.index_dist, "variant": args.variant, "prepare_backward": "call" if prepare else ("in forward" if in_forward else False),
                    "lookups_per_step": N_avg},
         "roofline": {"bound": dk["bound"], "kernel": dk["kernel"], "achieved": dk["achieved"],
                      "peak": dk["peak"], "unit": "GB/s", "frac": dk["frac"],

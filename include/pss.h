@@ -70,8 +70,14 @@
  *     invalid with ATOMIC or SPARSE (PSS_ERR_UNSUPPORTED).
  *   PSS_PREPARE_BACKWARD  read by pss_forward only (the other calls ignore
  *     it; pss_prepare_backward does the same work as a call of its own): the
- *     forward also groups the batch's lookups by token for the backward, on
- *     a library-owned stream that runs beside the forward kernel.  The next
+ *     forward also groups the batch's lookups by token for the backward.  A
+ *     forward that runs its streamed kernel (one item per bag, d in {64,
+ *     128, 256}, Z % 4 == 0, the shared array within 32 MiB) writes the
+ *     grouping's first stage (every lookup's key and pooled row, and the
+ *     first radix pass's digit counts) from that kernel, on `stream`, while
+ *     it reads the batch's index and offset entries; the backward finishes
+ *     the grouping on its stream.  Other forwards group the batch on a
+ *     library-owned stream that runs beside the forward kernel.  The next
  *     pss_backward_update on the same stream uses that grouping when its
  *     indices and offsets pointers, batch shape, hash parameters and options
  *     match and it runs the SORTED variant grouped by token (AUTO's choice
@@ -105,7 +111,8 @@
  *   library-owned device buffer kept per (device, stream) between calls and
  *   grown to the largest call made on that stream (taken from a
  *   library-owned memory pool), and so does a forward call with
- *   PSS_PREPARE_BACKWARD, together with a library stream and two events;
+ *   PSS_PREPARE_BACKWARD (with a library stream and two events when the
+ *   grouping runs on the library's stream);
  *   pss_release_scratch returns all of these.
  *   While `stream` is being captured into a graph, scratch is allocated
  *   stream-ordered from the pool and freed on the same stream instead, so

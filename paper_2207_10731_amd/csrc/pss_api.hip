@@ -255,6 +255,12 @@ class CallScratch {
 // grouping again.  A later prepare on the same stream reuses the buffer: its
 // grouping waits for `start`, recorded after every earlier call on the
 // caller's stream (including the backward that read the buffer).
+//
+// A forward that runs the streamed kernel writes the grouping's first stage
+// (keygen) itself instead (`fused`): it reads the batch's index and offset
+// entries anyway.  Everything then happens on the caller's stream (no side
+// stream, no events), and the backward finishes the grouping (the radix
+// pass) before its reduction.
 struct Prepared {
   std::mutex mu;
   hipStream_t side = nullptr;
@@ -263,6 +269,7 @@ struct Prepared {
   void* buf = nullptr;
   size_t bytes = 0;
   bool valid = false;  // a grouping waits for its backward
+  bool fused = false;  // valid: its keygen stage was written by the forward kernel
   const void* indices = nullptr;
   const void* offsets = nullptr;
   KParams made{};
@@ -299,11 +306,12 @@ int prepare_backward(const KParams& p, const void* indices, const void* offsets,
   // A grouping that no backward used is dropped; the caller's stream first
   // waits for it, so that work the caller orders after this call (freeing or
   // refilling the old batch's indices) also follows the old grouping's reads.
-  if (pr->valid && hipStreamWaitEvent(stream, pr->ready, 0) != hipSuccess) {
+  if (pr->valid && !pr->fused && hipStreamWaitEvent(stream, pr->ready, 0) != hipSuccess) {
     pr->valid = false;
     return PSS_ERR_HIP;
   }
   pr->valid = false;
+  pr->fused = false;
   // created on first use (each one again if an earlier creation failed);
   // both events order work on this device only, so they release at device
   // scope (a system-scope release would write back the L2s for the host)
@@ -344,6 +352,65 @@ int prepare_backward(const KParams& p, const void* indices, const void* offsets,
   return PSS_OK;
 }
 
+// Sets up the slot for a grouping whose keygen stage the streamed forward
+// kernel writes on the caller's stream (the buffer is allocated, and an
+// unused earlier grouping dropped, in stream order); *kg gets the stage's
+// layout in the slot's buffer.  The slot becomes valid only through
+// mark_fused, once the forward kernel has been enqueued.
+int prepare_fused(const KParams& p, const void* indices, const void* offsets, hipStream_t stream,
+                  pss::KeygenOut* kg, Prepared** slot) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return PSS_ERR_HIP;
+  Prepared* pr = nullptr;
+  {
+    std::lock_guard<std::mutex> map_lock(g_prep_mu);
+    pr = &g_prep[{dev, reinterpret_cast<uintptr_t>(stream)}];
+  }
+  std::lock_guard<std::mutex> lock(pr->mu);
+  // an unused grouping made on the library stream may still be reading its
+  // batch or writing the buffer: the caller's stream waits for it
+  if (pr->valid && !pr->fused && hipStreamWaitEvent(stream, pr->ready, 0) != hipSuccess) {
+    pr->valid = false;
+    return PSS_ERR_HIP;
+  }
+  pr->valid = false;
+  pr->fused = false;
+  const size_t need = pss::sorted_workspace_bytes(p);
+  if (pr->bytes < need) {
+    if (pr->buf != nullptr && hipFreeAsync(pr->buf, stream) != hipSuccess) return PSS_ERR_HIP;
+    pr->buf = nullptr;
+    pr->bytes = 0;
+    const int st = scratch_alloc(&pr->buf, need, stream);
+    if (st != PSS_OK) {
+      pr->buf = nullptr;
+      return st;
+    }
+    pr->bytes = need;
+  }
+  *kg = pss::keygen_layout(p, pr->buf);
+  pr->indices = indices;
+  pr->offsets = offsets;
+  pr->made = p;
+  *slot = pr;
+  return PSS_OK;
+}
+
+void mark_fused(Prepared* pr) {
+  std::lock_guard<std::mutex> lock(pr->mu);
+  pr->valid = true;
+  pr->fused = true;
+}
+
+// The grouped pairs of a prepared grouping, on `stream`: wait for the
+// library stream's grouping, or finish the one whose keygen stage the
+// forward wrote.
+hipError_t prepared_pairs(Prepared* prep, const KParams& p, hipStream_t stream,
+                          pss::GroupedPairs* pairs) {
+  if (prep->fused) return pss::finish_group_sorted(p, prep->buf, true, stream, pairs);
+  *pairs = prep->pairs;
+  return hipStreamWaitEvent(stream, prep->ready, 0);
+}
+
 // The grouping prepared by the last forward on `stream`, if it was made for
 // this batch and `usable`; nullptr otherwise.  A prepared grouping serves the
 // next backward call on its stream only: this call drops it either way.  On
@@ -365,7 +432,7 @@ Prepared* take_prepared(hipStream_t stream, const void* indices, const void* off
   std::unique_lock<std::mutex> slot(pr->mu);
   const bool match = pr->valid && pr->indices == indices && pr->offsets == offsets &&
                      same_grouping(pr->made, p);
-  if (pr->valid && (!match || !usable)) {
+  if (pr->valid && !pr->fused && (!match || !usable)) {
     // dropped unused: the caller's stream waits for the grouping (it may
     // still be reading its batch's indices and offsets)
     if (hipStreamWaitEvent(stream, pr->ready, 0) != hipSuccess) (void)hipGetLastError();
@@ -471,9 +538,9 @@ hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state
     pss::GroupedPairs pairs;
     hipError_t e = hipSuccess;
     if (prep != nullptr) {
-      // the grouping ran on the library stream during the forward
-      e = hipStreamWaitEvent(stream, prep->ready, 0);
-      pairs = prep->pairs;
+      // the grouping made ahead (on the library stream, or begun by the
+      // forward kernel)
+      e = prepared_pairs(prep, p, stream, &pairs);
     } else {
       e = pss::launch_group_sorted(p, indices, offsets, group_ws, stream, &pairs);
     }
@@ -497,9 +564,11 @@ hipError_t enqueue_backward(const BackwardPlan& plan, void* shared, float* state
   }
   if (!plan.fused) e = pss::launch_zero(dst, M, stream);
   if (e == hipSuccess && prep != nullptr) {
-    // the grouping ran on the library stream during the forward
-    e = hipStreamWaitEvent(stream, prep->ready, 0);
-    if (e == hipSuccess) e = pss::launch_reduce_sorted(dst, scale, p, prep->pairs, grad_out, stream);
+    // the grouping made ahead (on the library stream, or begun by the
+    // forward kernel)
+    pss::GroupedPairs pairs;
+    e = prepared_pairs(prep, p, stream, &pairs);
+    if (e == hipSuccess) e = pss::launch_reduce_sorted(dst, scale, p, pairs, grad_out, stream);
   } else if (e == hipSuccess) {
     e = plan.variant == PSS_BWD_SORTED
             ? pss::launch_deposit_sorted(dst, scale, p, indices, offsets, grad_out, sort_ws, stream)
@@ -580,12 +649,26 @@ int pss_forward(const void* shared, int64_t M, int32_t Z, int32_t d,
   // capture.  The preparation only saves the backward some work: if it cannot be set
   // up (no memory for its buffer, a failed runtime call), the forward runs
   // anyway and the backward groups the batch itself.
+  const bool bf16 = hash_params->weight_dtype == PSS_BF16;
+  pss::KeygenOut kg;
+  Prepared* fused = nullptr;
   if ((hash_params->flags & PSS_PREPARE_BACKWARD) && p.N > 0 && groups_by_token(M, p, hash_params) &&
       !capturing(stream)) {
-    if (prepare_backward(p, indices, offsets, stream) != PSS_OK) (void)hipGetLastError();
+    // the streamed kernel writes the grouping's keygen stage itself; other
+    // forwards leave the grouping to the library stream
+    if (pss::forward_streams(p, bf16)) {
+      if (prepare_fused(p, indices, offsets, stream, &kg, &fused) != PSS_OK) {
+        (void)hipGetLastError();
+        fused = nullptr;
+      }
+    } else if (prepare_backward(p, indices, offsets, stream) != PSS_OK) {
+      (void)hipGetLastError();
+    }
   }
-  return hip_status(pss::launch_forward(shared, hash_params->weight_dtype == PSS_BF16, p, indices,
-                                        offsets, out, stream));
+  const hipError_t e = pss::launch_forward(shared, bf16, p, indices, offsets, out, stream,
+                                           fused != nullptr ? &kg : nullptr);
+  if (e == hipSuccess && fused != nullptr) mark_fused(fused);
+  return hip_status(e);
 }
 
 int pss_prepare_backward(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash_params,

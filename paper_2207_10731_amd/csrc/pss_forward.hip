@@ -21,6 +21,7 @@
 // chunks of factor 0; mean pooling divides a finished row by the bag's item
 // count; rows may be stored as bfloat16 (round to nearest even); indices and
 // offsets may be int32.
+#include "pss_keygen.hpp"
 #include "pss_launch.hpp"
 
 namespace pss {
@@ -398,7 +399,8 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
 template <typename WT, int PPU, bool SIGN, bool I32>
 __global__ __launch_bounds__(kBlockThreads) void forward_stream_kernel(
     const WT* __restrict__ w, const KParams p, const void* __restrict__ indices,
-    const void* __restrict__ offsets, void* __restrict__ out, const uint32_t nx) {
+    const void* __restrict__ offsets, void* __restrict__ out, const uint32_t nx,
+    const KeygenOut kg) {
   constexpr int D = stream_group<PPU>();
   const int lane = threadIdx.x & (kWave - 1);
   // Workgroups go round-robin to the XCDs (grid.x is a multiple of nx).
@@ -420,8 +422,23 @@ __global__ __launch_bounds__(kBlockThreads) void forward_stream_kernel(
   // caches instead of sending scattered reads to HBM in the middle of the
   // write stream.  In a training step (entries not cached after the
   // backward) this took the headline forward from 189 to 171 us.
+  //
+  // With kg (the backward's grouping prepared by this forward), the same
+  // entries are read by the grouping's keygen instead (keygen_tile: the
+  // (h0, row) pairs and the first radix pass's digit counts of every sort
+  // tile), which then serves as the prefetch.  XCD x's workgroups take the
+  // contiguous x-th eighth of the sort tiles, about the tables it owns.
   uint32_t pf = 0;
-  {
+  __shared__ KeygenLds kg_lds;
+  if (kg.keys != nullptr) {
+    const uint32_t per_x = (kg.nblocks + nx - 1) / nx;
+    const uint32_t lo = sm.x * per_x;
+    const uint32_t hi = lo + per_x < kg.nblocks ? lo + per_x : kg.nblocks;
+    const uint32_t wgs = gridDim.x / nx, rank = blockIdx.x / nx;
+    for (uint32_t tile = lo + rank; tile < hi; tile += wgs)
+      keygen_tile<I32, false>(p, indices, offsets, kg.keys, kg.rows, kg.inv_len, kg.counts,
+                              kg.nblocks, tile, kg_lds);
+  } else {
     const uint64_t t_lo = static_cast<uint64_t>(sm.x) * sm.K / sm.L;
     const uint64_t t_hi = (static_cast<uint64_t>(sm.x + 1) * sm.K - 1) / sm.L + 1;  // <= T
     const uint64_t g_lo = t_lo * p.B, g_hi = t_hi * p.B;
@@ -589,25 +606,27 @@ static uint32_t stream_blocks(uint64_t units) {
 
 template <typename WT, int PPU, bool SIGN>
 static hipError_t launch_stream_t(const WT* w, const KParams& p, const void* indices,
-                                  const void* offsets, void* out, hipStream_t stream) {
+                                  const void* offsets, void* out, hipStream_t stream,
+                                  const KeygenOut& kg) {
   const uint64_t units = (p.num_bags * p.d + kWave * 4 - 1) / (kWave * 4);
   const uint32_t blocks = stream_blocks(units);
   const uint32_t nx = blocks % kXcds == 0 ? kXcds : 1u;
   if (p.idx32)
     hipLaunchKernelGGL((forward_stream_kernel<WT, PPU, SIGN, true>), dim3(blocks),
-                       dim3(kBlockThreads), 0, stream, w, p, indices, offsets, out, nx);
+                       dim3(kBlockThreads), 0, stream, w, p, indices, offsets, out, nx, kg);
   else
     hipLaunchKernelGGL((forward_stream_kernel<WT, PPU, SIGN, false>), dim3(blocks),
-                       dim3(kBlockThreads), 0, stream, w, p, indices, offsets, out, nx);
+                       dim3(kBlockThreads), 0, stream, w, p, indices, offsets, out, nx, kg);
   return hipGetLastError();
 }
 
 template <typename WT, bool SIGN>
 static hipError_t launch_stream_s(const WT* w, const KParams& p, const void* indices,
-                                  const void* offsets, void* out, hipStream_t stream) {
-  if (p.d == 64) return launch_stream_t<WT, 4, SIGN>(w, p, indices, offsets, out, stream);
-  if (p.d == 128) return launch_stream_t<WT, 2, SIGN>(w, p, indices, offsets, out, stream);
-  return launch_stream_t<WT, 1, SIGN>(w, p, indices, offsets, out, stream);
+                                  const void* offsets, void* out, hipStream_t stream,
+                                  const KeygenOut& kg) {
+  if (p.d == 64) return launch_stream_t<WT, 4, SIGN>(w, p, indices, offsets, out, stream, kg);
+  if (p.d == 128) return launch_stream_t<WT, 2, SIGN>(w, p, indices, offsets, out, stream, kg);
+  return launch_stream_t<WT, 1, SIGN>(w, p, indices, offsets, out, stream, kg);
 }
 
 template <typename WT, int EPL, int U, bool TAB, bool SIGN>
@@ -646,20 +665,29 @@ static hipError_t launch_fwd_s(const WT* w, const KParams& p, const void* indice
 
 template <typename WT>
 static hipError_t launch_fwd_w(const WT* w, const KParams& p, const void* indices,
-                               const void* offsets, void* out, hipStream_t stream) {
+                               const void* offsets, void* out, hipStream_t stream,
+                               const KeygenOut* kg) {
   if (stream_applies<WT>(p)) {
-    if (p.sign_mode) return launch_stream_s<WT, true>(w, p, indices, offsets, out, stream);
-    return launch_stream_s<WT, false>(w, p, indices, offsets, out, stream);
+    const KeygenOut none{};
+    const KeygenOut& k = kg != nullptr ? *kg : none;
+    if (p.sign_mode) return launch_stream_s<WT, true>(w, p, indices, offsets, out, stream, k);
+    return launch_stream_s<WT, false>(w, p, indices, offsets, out, stream, k);
   }
+  if (kg != nullptr) return hipErrorInvalidValue;  // only the streamed kernel writes a keygen
   if (p.sign_mode) return launch_fwd_s<WT, true>(w, p, indices, offsets, out, stream);
   return launch_fwd_s<WT, false>(w, p, indices, offsets, out, stream);
 }
 
+bool forward_streams(const KParams& p, bool bf16) {
+  return bf16 ? stream_applies<uint16_t>(p) : stream_applies<float>(p);
+}
+
 hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const void* indices,
-                          const void* offsets, void* out, hipStream_t stream) {
+                          const void* offsets, void* out, hipStream_t stream,
+                          const KeygenOut* kg) {
   if (bf16)
-    return launch_fwd_w(static_cast<const uint16_t*>(w), p, indices, offsets, out, stream);
-  return launch_fwd_w(static_cast<const float*>(w), p, indices, offsets, out, stream);
+    return launch_fwd_w(static_cast<const uint16_t*>(w), p, indices, offsets, out, stream, kg);
+  return launch_fwd_w(static_cast<const float*>(w), p, indices, offsets, out, stream, kg);
 }
 
 }  // namespace pss

@@ -8,11 +8,25 @@
 
 namespace pss {
 
+// First stage of the grouping (keys, rows, the first radix pass's digit
+// counts, inv_len with mean pooling) as laid out in its workspace; the
+// streamed forward can write it (keys == nullptr: not requested).
+struct KeygenOut {
+  uint32_t* keys = nullptr;
+  uint32_t* rows = nullptr;
+  float* inv_len = nullptr;
+  uint32_t* counts = nullptr;
+  uint32_t nblocks = 0;
+};
 // Forward: pooled rows of every bag into out[B][T*d].
 // indices / offsets are int64 (int32 when p.idx32); out / grad rows are
-// float32 (bfloat16 when p.rows_bf16).
+// float32 (bfloat16 when p.rows_bf16).  With kg (streamed kernel only, see
+// forward_streams) the kernel also writes the grouping's first stage there.
 hipError_t launch_forward(const void* w, bool bf16, const KParams& p, const void* indices,
-                          const void* offsets, void* out, hipStream_t stream);
+                          const void* offsets, void* out, hipStream_t stream,
+                          const KeygenOut* kg = nullptr);
+// Whether the forward of this batch runs the streamed kernel.
+bool forward_streams(const KParams& p, bool bf16);
 
 // Atomic deposit: dst[addr] += scale * grad for every (item, dim).
 hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, const void* indices,
@@ -34,6 +48,11 @@ struct GroupedPairs {
   const uint32_t* rows = nullptr;  // its pooled row b*T + t
   const float* inv_len = nullptr;  // 1 / |bag| per pooled row (mean pooling)
 };
+KeygenOut keygen_layout(const KParams& p, void* workspace);
+// The rest of the grouping once its first stage is in the workspace
+// (first_counted: the first pass's digit counts are there too).
+hipError_t finish_group_sorted(const KParams& p, void* workspace, bool first_counted,
+                               hipStream_t stream, GroupedPairs* out);
 hipError_t launch_group_sorted(const KParams& p, const void* indices, const void* offsets,
                                void* workspace, hipStream_t stream, GroupedPairs* out);
 // Events recorded around every later reduce-and-deposit launch (both null:

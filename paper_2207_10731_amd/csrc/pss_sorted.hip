@@ -25,15 +25,11 @@
 //             sum per piece.
 #include <atomic>
 
+#include "pss_keygen.hpp"
 #include "pss_launch.hpp"
 
 namespace pss {
 
-constexpr int kSortBits = 8;
-constexpr int kBins = 1 << kSortBits;
-constexpr int kSortItemsPerLane = 8;
-constexpr int kSortTile = kBlockThreads * kSortItemsPerLane;  // keys per block
-constexpr int kWaveSortKeys = kWave * kSortItemsPerLane;       // keys per wave
 constexpr int kDigitsPerThread = kBins / kBlockThreads;
 static_assert(kBins % kBlockThreads == 0, "whole digits per thread in the scatter prologue");
 
@@ -175,20 +171,8 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
   }
 }
 
-// indices[e] / offsets[g] with the integer width fixed at compile time.
-template <bool I32>
-__device__ __forceinline__ int64_t load_int(const void* a, uint64_t i) {
-  if constexpr (I32) return __builtin_nontemporal_load(static_cast<const int32_t*>(a) + i);
-  else return __builtin_nontemporal_load(static_cast<const int64_t*>(a) + i);
-}
-
 // Keygen in item space for batches with as many items as bags, fused with
-// the first radix pass's histogram: workgroup blk takes the sort tile of
-// items [tile * kSortTile, ...), writes their (key, row) pairs and the tile's
-// digit counts of the low kSortBits bits (counts[d * nblocks + tile]).  When
-// every item of the tile is its own bag (offsets[e] == e), item e belongs
-// to bag e; otherwise each item finds its bag by binary search over the
-// offsets (the largest g with offsets[g] <= e).
+// the first radix pass's histogram: one sort tile per workgroup (keygen_tile).
 template <bool I32>
 __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
@@ -196,81 +180,8 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     uint32_t* __restrict__ counts, const uint32_t nblocks, const uint32_t per_xcd) {
   const uint32_t tile = sort_tile_index(per_xcd);
   if (tile >= nblocks) return;
-  const int64_t tile0 = static_cast<int64_t>(tile) * kSortTile;
-  const int in_tile = p.N - tile0 < kSortTile ? static_cast<int>(p.N - tile0) : kSortTile;
-  __shared__ uint32_t hist[kWavesPerBlock][kBins];
-  __shared__ int irregular;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
-  const int lbase = w * kWaveSortKeys;
-  // Every index and offset of the thread is requested before any is used:
-  // one wait for memory per thread.  An item's index does not depend on its
-  // bag.
-  uint32_t ix[kSortItemsPerLane];
-  int64_t ofs[kSortItemsPerLane];
-#pragma unroll
-  for (int s = 0; s < kSortItemsPerLane; ++s) {
-    const int li = lbase + s * kWave + lane;
-    const int64_t e = tile0 + li;
-    ix[s] = 0;
-    ofs[s] = e;
-    if (li < in_tile) {
-      ix[s] = static_cast<uint32_t>(load_int<I32>(indices, static_cast<uint64_t>(e)));
-      ofs[s] = load_int<I32>(offsets, static_cast<uint64_t>(e));
-    }
-  }
-  const int64_t end = tile0 + in_tile;
-  const int64_t oend = threadIdx.x == 0 ? load_int<I32>(offsets, static_cast<uint64_t>(end)) : end;
-  for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads) (&hist[0][0])[i] = 0;
-  if (threadIdx.x == 0) irregular = 0;
-  __syncthreads();
-  bool mine_ok = oend == end;
-#pragma unroll
-  for (int s = 0; s < kSortItemsPerLane; ++s)
-    if (ofs[s] != tile0 + lbase + s * kWave + lane) mine_ok = false;
-  if (!mine_ok) irregular = 1;
-  __syncthreads();
-  const bool onehot = irregular == 0;
-#pragma unroll
-  for (int s = 0; s < kSortItemsPerLane; ++s) {
-    const int li = lbase + s * kWave + lane;
-    const bool valid = li < in_tile;
-    uint32_t digit = 0;
-    if (valid) {
-      const int64_t e = tile0 + li;
-      // bag numbers are below 2^32
-      uint32_t g = static_cast<uint32_t>(e);
-      float il = 1.f;
-      bool first = true;
-      if (!onehot) {
-        uint64_t lo = 0, hi = p.num_bags - 1;  // largest g with offsets[g] <= e
-        while (lo < hi) {
-          const uint64_t mid = (lo + hi + 1) >> 1;
-          if (load_int<I32>(offsets, mid) <= e) lo = mid; else hi = mid - 1;
-        }
-        g = static_cast<uint32_t>(lo);
-        const int64_t s0 = load_int<I32>(offsets, lo);
-        const int64_t s1 = load_int<I32>(offsets, lo + 1);
-        first = s0 == e;
-        il = s1 > s0 ? 1.f / static_cast<float>(s1 - s0) : 1.f;
-      }
-      const uint32_t t = g / p.B;
-      const uint32_t b = g - t * p.B;
-      const uint32_t r = b * p.T + t;
-      const uint32_t key = item_hash(ix[s], t * p.C, p.TC, p.a, p.b);
-      keys[e] = key;
-      rows[e] = r;
-      if (p.mean && first) inv_len[r] = il;
-      digit = key & (kBins - 1);
-    }
-    if (valid) atomicAdd(&hist[w][digit], 1u);
-  }
-  __syncthreads();
-  for (int d = threadIdx.x; d < kBins; d += kBlockThreads) {
-    uint32_t c = 0;
-#pragma unroll
-    for (int ww = 0; ww < kWavesPerBlock; ++ww) c += hist[ww][d];
-    counts[static_cast<uint64_t>(d) * nblocks + tile] = c;
-  }
+  __shared__ KeygenLds lds;
+  keygen_tile<I32, true>(p, indices, offsets, keys, rows, inv_len, counts, nblocks, tile, lds);
 }
 
 // Scans of the count rows.  A chunk of kScanChunk consecutive entries is
@@ -986,44 +897,67 @@ static hipError_t launch_reduce_g(float* dst, float scale, const KParams& p, con
   return launch_reduce_s<false, GT, REC>(dst, scale, p, keys, rows, grad, il, rk, rv, stream);
 }
 
+// Workspace of the grouping: k0, v0, k1, v1 (N words each), the radix
+// scratch (digit counts first), then inv_len (mean pooling).
+KeygenOut keygen_layout(const KParams& p, void* workspace) {
+  const int64_t N = p.N;
+  uint32_t* k0 = static_cast<uint32_t*>(workspace);
+  uint32_t* scratch = k0 + 4 * N;
+  KeygenOut kg;
+  kg.keys = k0;
+  kg.rows = k0 + N;
+  kg.inv_len = p.mean ? reinterpret_cast<float*>(reinterpret_cast<char*>(scratch) +
+                                                 radix_scratch_bytes(N))
+                      : nullptr;
+  kg.counts = scratch;
+  kg.nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
+  return kg;
+}
+
+hipError_t finish_group_sorted(const KParams& p, void* workspace, bool first_counted,
+                               hipStream_t stream, GroupedPairs* out) {
+  const int64_t N = p.N;
+  const KeygenOut kg = keygen_layout(p, workspace);
+  uint32_t* k0 = kg.keys;
+  uint32_t* v0 = kg.rows;
+  uint32_t* k1 = v0 + N;
+  uint32_t* v1 = k1 + N;
+  hipError_t e = hipSuccess;
+  if (N > 0)
+    e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), kg.counts, stream, nullptr,
+                         first_counted);
+  out->keys = k0;
+  out->rows = v0;
+  out->inv_len = kg.inv_len;
+  return e;
+}
+
 hipError_t launch_group_sorted(const KParams& p, const void* indices, const void* offsets,
                                void* workspace, hipStream_t stream, GroupedPairs* out) {
   const int64_t N = p.N;
-  uint32_t* k0 = static_cast<uint32_t*>(workspace);
-  uint32_t* v0 = k0 + N;
-  uint32_t* k1 = v0 + N;
-  uint32_t* v1 = k1 + N;
-  uint32_t* scratch = v1 + N;
-  float* inv_len = p.mean ? reinterpret_cast<float*>(
-                                reinterpret_cast<char*>(scratch) + radix_scratch_bytes(N))
-                          : nullptr;
-  out->keys = k0;
-  out->rows = v0;
-  out->inv_len = inv_len;
-  if (N == 0) return hipSuccess;
+  const KeygenOut kg = keygen_layout(p, workspace);
+  if (N == 0) return finish_group_sorted(p, workspace, false, stream, out);
   // As many items as bags (one-hot batches): keygen in item space, fused
   // with the first pass's histogram.
   const bool item_space = static_cast<uint64_t>(N) == p.num_bags;
   hipError_t e = hipSuccess;
   if (item_space) {
-    const uint32_t nblocks = static_cast<uint32_t>((N + kSortTile - 1) / kSortTile);
-    const uint32_t per_xcd = sort_tiles_per_xcd(nblocks);
+    const uint32_t per_xcd = sort_tiles_per_xcd(kg.nblocks);
     const dim3 grid(per_xcd * static_cast<uint32_t>(kXcds));
     if (p.idx32)
       hipLaunchKernelGGL(keygen_hist_kernel<true>, grid, dim3(kBlockThreads), 0, stream, p,
-                         indices, offsets, k0, v0, inv_len, scratch, nblocks, per_xcd);
+                         indices, offsets, kg.keys, kg.rows, kg.inv_len, kg.counts, kg.nblocks,
+                         per_xcd);
     else
       hipLaunchKernelGGL(keygen_hist_kernel<false>, grid, dim3(kBlockThreads), 0, stream, p,
-                         indices, offsets, k0, v0, inv_len, scratch, nblocks, per_xcd);
+                         indices, offsets, kg.keys, kg.rows, kg.inv_len, kg.counts, kg.nblocks,
+                         per_xcd);
     e = hipGetLastError();
   } else {
-    e = launch_keygen(p, indices, offsets, k0, v0, inv_len, stream);
+    e = launch_keygen(p, indices, offsets, kg.keys, kg.rows, kg.inv_len, stream);
   }
-  if (e == hipSuccess)
-    e = radix_sort_pairs(k0, v0, k1, v1, N, grouping_bits(N), scratch, stream, nullptr, item_space);
-  out->keys = k0;
-  out->rows = v0;
-  return e;
+  if (e != hipSuccess) return e;
+  return finish_group_sorted(p, workspace, item_space, stream, out);
 }
 
 hipError_t launch_reduce_sorted(float* dst, float scale, const KParams& p, const GroupedPairs& g,

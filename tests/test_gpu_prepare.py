@@ -1,11 +1,14 @@
-"""PSS_PREPARE_BACKWARD: the forward groups the batch on a library stream for
-the next backward on the same stream.  Every result is checked against the
-oracle, including the cases where the prepared grouping must not be used."""
+"""PSS_PREPARE_BACKWARD: the forward groups the batch for the next backward on
+the same stream, on a library stream, or (when it runs the streamed kernel)
+by writing the grouping's keygen stage itself.  Every result is checked
+against the oracle, including the cases where the prepared grouping must not
+be used."""
 import numpy as np
 import pytest
 import torch
 
 import synth
+from synth.gen import Inputs
 from paper_2207_10731_amd import pss
 import parity
 from parity import Layer
@@ -208,3 +211,113 @@ def test_prepared_on_two_streams():
     for L, out, g in zip(Ls, outs, gs):
         _check_forward(L, out.cpu().numpy())
         _check_update(L, g)
+
+
+
+# The streamed forward (one item per bag, d in {64, 128, 256}, Z % 4 == 0,
+# array within the aggregate L2) writes the keygen stage of the grouping; the
+# backward finishes it.  Shapes: the XCD groups' share of the sort tiles,
+# ragged last tiles, a grid too small for the XCD groups.
+FUSED = {
+    "c2-700": dict(key="c2", B=700),
+    "c2-4000": dict(key="c2", B=4000),        # 51 sort tiles over 8 XCD groups
+    "d64-t7": dict(key="c2", B=1001, T=7, d=64, Z=16, M=1_000_000),
+    "small-grid": dict(key="c2", B=20, T=2, M=50_000),
+}
+
+
+def _fused_layer(case, **kw):
+    c = dict(FUSED[case])
+    wl = synth.get(c.pop("key"))
+    B = c.pop("B")
+    if c:
+        wl = wl.scaled(**c)
+    return Layer(wl, B=B, **kw)
+
+
+@pytest.mark.parametrize("case", list(FUSED))
+@pytest.mark.parametrize("opt", ["plain", "i32", "mean", "sign"])
+def test_fused_keygen_step(case, opt):
+    kw = {"plain": {}, "i32": dict(idx32=True), "mean": dict(mean=True),
+          "sign": dict(sign="sparse")}[opt]
+    print(f"fused keygen case {case} {opt}", flush=True)
+    L = _fused_layer(case, flags=pss.PSS_BWD_SORTED | PREP, **kw)
+    g = synth.make_grad(L.wl, B=L.B)
+    _check_forward(L, L.forward())
+    L.backward(g)
+    _check_update(L, g)
+
+
+def _irregular(T, B, seed, k, n_index=50_000):
+    """N == T*B items, but k empty bags and k bags of two items: the
+    streamed forward's slow path, and the keygen's bag search."""
+    rng = np.random.default_rng(seed)
+    pick = rng.permutation(T * B)
+    lengths = np.ones(T * B, dtype=np.int64)
+    lengths[pick[:k]] = 0
+    lengths[pick[k:2 * k]] = 2
+    offsets = np.zeros(T * B + 1, dtype=np.int64)
+    np.cumsum(lengths, out=offsets[1:])
+    indices = rng.integers(0, n_index, size=int(offsets[-1]), dtype=np.int64)
+    return indices, offsets
+
+
+@pytest.mark.parametrize("mean", [False, True])
+def test_fused_keygen_irregular_bags(mean):
+    """As many items as bags but not one per bag: the forward still streams
+    and writes the keygen stage, whose items search their bags."""
+    wl = synth.get("c2").scaled(T=6, M=700_000)
+    L = Layer(wl, B=900, flags=pss.PSS_BWD_SORTED | PREP, mean=mean)
+    indices, offsets = _irregular(wl.T, L.B, 5, 300)
+    L.x = Inputs(indices=indices, offsets=offsets, B=L.B)
+    L.indices = torch.from_numpy(indices).to(L.dev)
+    L.offsets = torch.from_numpy(offsets).to(L.dev)
+    g = synth.make_grad(wl, B=L.B)
+    _check_forward(L, L.forward())
+    L.backward(g)
+    _check_update(L, g)
+
+
+def test_fused_keygen_bf16_storage_and_adagrad():
+    """The fused stage serves the backward whatever the update: bf16 storage
+    with SGD (G buffer and optimizer pass), and Adagrad."""
+    wl = synth.get("c2").scaled(T=8, M=1_000_000)
+    for w in (wl.scaled(weight_dtype="bf16"), wl.scaled(optimizer="adagrad", lr=0.01)):
+        L = Layer(w, B=600, flags=pss.PSS_BWD_SORTED | PREP, s0=0.1)
+        g = synth.make_grad(w, B=L.B)
+        _check_forward(L, L.forward())
+        L.backward(g)
+        _check_update(L, g)
+
+
+def test_fused_keygen_run_sums_by_address():
+    """Whole-row chunks with the deposit by address (run sums by address):
+    the backward finishes the fused grouping, then deposits by address."""
+    wl = synth.get("c2").scaled(T=5, Z=128, M=300_000)
+    L = Layer(wl, B=800, flags=pss.PSS_BWD_SORTED | PREP | pss.PSS_DEPOSIT_BY_ADDRESS)
+    g = synth.make_grad(wl, B=L.B)
+    _check_forward(L, L.forward())
+    L.backward(g)
+    _check_update(L, g)
+
+
+def test_fused_keygen_after_explicit_prepare():
+    """pss_prepare_backward (library stream), then the forward with the flag
+    for the same batch (its keygen replaces the library stream's grouping,
+    after waiting for it), then the backward."""
+    L = _fused_layer("c2-700", flags=PREP)
+    wl = L.wl
+    g = synth.make_grad(wl, B=L.B)
+    pss.pss_prepare_backward(wl.M, wl.Z, wl.d, L.hp, L.indices, L.offsets)
+    _check_forward(L, L.forward())
+    L.backward(g)
+    _check_update(L, g)
+    # and the other way round: a fused stage left unused, then an explicit
+    # preparation and a forward without the flag
+    M2 = Layer(wl, B=L.B, batch=1)
+    g2 = synth.make_grad(wl, B=M2.B, batch=1)
+    L.forward()
+    pss.pss_prepare_backward(wl.M, wl.Z, wl.d, M2.hp, M2.indices, M2.offsets)
+    _check_forward(M2, M2.forward())
+    M2.backward(g2)
+    _check_update(M2, g2)

@@ -110,8 +110,10 @@ def test_fullsize_backward_sampled_elements(key):
 
 @pytest.mark.parametrize("key", ["c2", "c3"])
 def test_fullsize_prepared_step(key):
-    """The bench's step: forward with PSS_PREPARE_BACKWARD (the grouping runs
-    beside the forward kernel), then the backward reusing it."""
+    """The bench's step: forward with PSS_PREPARE_BACKWARD, then the backward
+    reusing the grouping (one-hot: the streamed forward kernel writes its
+    keygen stage and the backward finishes it; multi-hot: the grouping runs
+    on the library's stream beside the forward kernel)."""
     F = Full(key, flags=pss.PSS_PREPARE_BACKWARD)
     wl = F.wl
     g, grad = _grad(F)

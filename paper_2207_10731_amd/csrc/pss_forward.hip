@@ -21,6 +21,8 @@
 // chunks of factor 0; mean pooling divides a finished row by the bag's item
 // count; rows may be stored as bfloat16 (round to nearest even); indices and
 // offsets may be int32.
+#include <atomic>
+
 #include "pss_keygen.hpp"
 #include "pss_launch.hpp"
 
@@ -424,7 +426,7 @@ __global__ __launch_bounds__(kBlockThreads) void forward_stream_kernel(
   // backward) this took the headline forward from 189 to 171 us.
   //
   // With kg (the backward's grouping prepared by this forward), the same
-  // entries are read by the grouping's keygen instead (keygen_tile: the
+  // entries are read by the grouping's keygen instead (keygen_process: the
   // (h0, row) pairs and the first radix pass's digit counts of every sort
   // tile), which then serves as the prefetch.  XCD x's workgroups take the
   // contiguous x-th eighth of the sort tiles, about the tables it owns.
@@ -435,9 +437,23 @@ __global__ __launch_bounds__(kBlockThreads) void forward_stream_kernel(
     const uint32_t lo = sm.x * per_x;
     const uint32_t hi = lo + per_x < kg.nblocks ? lo + per_x : kg.nblocks;
     const uint32_t wgs = gridDim.x / nx, rank = blockIdx.x / nx;
-    for (uint32_t tile = lo + rank; tile < hi; tile += wgs)
-      keygen_tile<I32, false>(p, indices, offsets, kg.keys, kg.rows, kg.inv_len, kg.counts,
-                              kg.nblocks, tile, kg_lds);
+    // the next tile's entries are requested before the current tile is
+    // worked (two input sets take turns)
+    KeygenIn ka, kb;
+    uint32_t tile = lo + rank;
+    if (tile < hi) keygen_load<I32, false>(p, indices, offsets, tile, ka);
+    while (tile < hi) {
+      const uint32_t t2 = tile + wgs;
+      if (t2 < hi) keygen_load<I32, false>(p, indices, offsets, t2, kb);
+      keygen_process<I32, false>(p, offsets, kg.keys, kg.rows, kg.inv_len, kg.counts, kg.nblocks,
+                                 tile, ka, kg_lds);
+      if (t2 >= hi) break;
+      const uint32_t t3 = t2 + wgs;
+      if (t3 < hi) keygen_load<I32, false>(p, indices, offsets, t3, ka);
+      keygen_process<I32, false>(p, offsets, kg.keys, kg.rows, kg.inv_len, kg.counts, kg.nblocks,
+                                 t2, kb, kg_lds);
+      tile = t3;
+    }
   } else {
     const uint64_t t_lo = static_cast<uint64_t>(sm.x) * sm.K / sm.L;
     const uint64_t t_hi = (static_cast<uint64_t>(sm.x + 1) * sm.K - 1) / sm.L + 1;  // <= T
@@ -448,10 +464,19 @@ __global__ __launch_bounds__(kBlockThreads) void forward_stream_kernel(
       if (g_lo >= hi_e) return;
       const uint64_t a0 = reinterpret_cast<uint64_t>(base);
       const uint64_t c_lo = (a0 + g_lo * es + 15) / 16, c_end = (a0 + hi_e * es) / 16;
-      for (uint64_t c = c_lo + static_cast<uint64_t>(sm.w) * kWave + lane; c < c_end;
-           c += static_cast<uint64_t>(sm.nw) * kWave) {
-        const uint4 v4 = *reinterpret_cast<const uint4*>(c * 16);
-        pf ^= v4.x ^ v4.y ^ v4.z ^ v4.w;
+      // kPrefetchBatch 16-byte pieces per lane requested before any is used
+      constexpr int kPrefetchBatch = 16;
+      const uint64_t stride = static_cast<uint64_t>(sm.nw) * kWave;
+      for (uint64_t c0 = c_lo + static_cast<uint64_t>(sm.w) * kWave + lane; c0 < c_end;
+           c0 += kPrefetchBatch * stride) {
+        uint4 v4[kPrefetchBatch];
+#pragma unroll
+        for (int k = 0; k < kPrefetchBatch; ++k) {
+          const uint64_t c = c0 + k * stride;
+          v4[k] = c < c_end ? *reinterpret_cast<const uint4*>(c * 16) : uint4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int k = 0; k < kPrefetchBatch; ++k) pf ^= v4[k].x ^ v4[k].y ^ v4[k].z ^ v4[k].w;
       }
     };
     touch(indices, static_cast<uint64_t>(p.N));
@@ -587,19 +612,34 @@ static bool stream_applies(const KParams& p) {
          p.num_bags * p.d < (1ull << 34);
 }
 
+// Compute units of each device, looked up once per device (callers may run
+// on several threads and devices).
+constexpr int kMaxDevices = 64;
+static std::atomic<int> g_cus[kMaxDevices];
+
+static int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int n = g_cus[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0) {
+      (void)hipGetLastError();
+      n = 256;
+    }
+    g_cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
 // Wavefronts of the streamed forward: one per SIMD (4 per compute unit).
 static uint32_t stream_blocks(uint64_t units) {
-  static int cus = 0;
-  if (cus <= 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-      cus = n;
-    else
-      cus = 256;
-  }
+  const uint64_t cus = static_cast<uint64_t>(device_cus());
   const uint64_t want = (units + kWavesPerBlock - 1) / kWavesPerBlock;
-  uint64_t blocks = want < static_cast<uint64_t>(cus) ? want : static_cast<uint64_t>(cus);
+  uint64_t blocks = want < cus ? want : cus;
   if (blocks >= kXcds) blocks = blocks / kXcds * kXcds;
   return static_cast<uint32_t>(blocks < 1 ? 1 : blocks);
 }

@@ -33,60 +33,77 @@ __device__ __forceinline__ int64_t load_int(const void* a, uint64_t i) {
   }
 }
 
-// LDS of keygen_tile.
+// LDS of keygen_process.
 struct KeygenLds {
   uint32_t hist[kWavesPerBlock][kBins];
   int irregular;
 };
 
-// Keygen of sort tile `tile` (items [tile * kSortTile, ...)) in item space,
-// for batches with as many items as bags, by the whole workgroup
-// (kBlockThreads threads; contains workgroup barriers, so every thread
-// calls it with the same tile).  When every item of the tile is its own bag
-// (offsets[e] == e), item e belongs to bag e; otherwise each item finds its
-// bag by binary search over the offsets (the largest g with offsets[g] <=
-// e).  With mean pooling it also writes inv_len[r] = 1 / |bag| for the row
-// of every nonempty bag whose first item lies in the tile.
+// Inputs of one sort tile, requested ahead of their use (keygen_load), so
+// that a workgroup can ask for its next tile's entries before it works on
+// the current one.
+struct KeygenIn {
+  uint32_t ix[kSortItemsPerLane];
+  int64_t ofs[kSortItemsPerLane];
+  int64_t oend;
+};
+
+// Requests the thread's indices and offsets of sort tile `tile` (items
+// [tile * kSortTile, ...)): every load is issued before any is used.  An
+// item's index does not depend on its bag.
 template <bool I32, bool NT>
-__device__ __forceinline__ void keygen_tile(const KParams& p, const void* __restrict__ indices,
-                                            const void* __restrict__ offsets,
-                                            uint32_t* __restrict__ keys,
-                                            uint32_t* __restrict__ rows,
-                                            float* __restrict__ inv_len,
-                                            uint32_t* __restrict__ counts, const uint32_t nblocks,
-                                            const uint32_t tile, KeygenLds& lds) {
+__device__ __forceinline__ void keygen_load(const KParams& p, const void* __restrict__ indices,
+                                            const void* __restrict__ offsets, const uint32_t tile,
+                                            KeygenIn& in) {
   const int64_t tile0 = static_cast<int64_t>(tile) * kSortTile;
   const int in_tile = p.N - tile0 < kSortTile ? static_cast<int>(p.N - tile0) : kSortTile;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
   const int lbase = w * kWaveSortKeys;
-  // Every index and offset of the thread is requested before any is used:
-  // one wait for memory per thread.  An item's index does not depend on its
-  // bag.
-  uint32_t ix[kSortItemsPerLane];
-  int64_t ofs[kSortItemsPerLane];
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s) {
     const int li = lbase + s * kWave + lane;
     const int64_t e = tile0 + li;
-    ix[s] = 0;
-    ofs[s] = e;
+    in.ix[s] = 0;
+    in.ofs[s] = e;
     if (li < in_tile) {
-      ix[s] = static_cast<uint32_t>(load_int<I32, NT>(indices, static_cast<uint64_t>(e)));
-      ofs[s] = load_int<I32, NT>(offsets, static_cast<uint64_t>(e));
+      in.ix[s] = static_cast<uint32_t>(load_int<I32, NT>(indices, static_cast<uint64_t>(e)));
+      in.ofs[s] = load_int<I32, NT>(offsets, static_cast<uint64_t>(e));
     }
   }
   const int64_t end = tile0 + in_tile;
-  const int64_t oend =
-      threadIdx.x == 0 ? load_int<I32, NT>(offsets, static_cast<uint64_t>(end)) : end;
+  in.oend = threadIdx.x == 0 ? load_int<I32, NT>(offsets, static_cast<uint64_t>(end)) : end;
+}
+
+// Keygen of sort tile `tile` in item space, for batches with as many items
+// as bags, from its requested inputs, by the whole workgroup (kBlockThreads
+// threads; contains workgroup barriers, so every thread calls it with the
+// same tile).  When every item of the tile is its own bag (offsets[e] == e),
+// item e belongs to bag e; otherwise each item finds its bag by binary
+// search over the offsets (the largest g with offsets[g] <= e).  With mean
+// pooling it also writes inv_len[r] = 1 / |bag| for the row of every
+// nonempty bag whose first item lies in the tile.
+template <bool I32, bool NT>
+__device__ __forceinline__ void keygen_process(const KParams& p, const void* __restrict__ offsets,
+                                               uint32_t* __restrict__ keys,
+                                               uint32_t* __restrict__ rows,
+                                               float* __restrict__ inv_len,
+                                               uint32_t* __restrict__ counts,
+                                               const uint32_t nblocks, const uint32_t tile,
+                                               const KeygenIn& in, KeygenLds& lds) {
+  const int64_t tile0 = static_cast<int64_t>(tile) * kSortTile;
+  const int in_tile = p.N - tile0 < kSortTile ? static_cast<int>(p.N - tile0) : kSortTile;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & (kWave - 1);
+  const int lbase = w * kWaveSortKeys;
+  const int64_t end = tile0 + in_tile;
   __syncthreads();  // a previous tile of this workgroup is done with the LDS
   for (int i = threadIdx.x; i < kWavesPerBlock * kBins; i += kBlockThreads)
     (&lds.hist[0][0])[i] = 0;
   if (threadIdx.x == 0) lds.irregular = 0;
   __syncthreads();
-  bool mine_ok = oend == end;
+  bool mine_ok = in.oend == end;
 #pragma unroll
   for (int s = 0; s < kSortItemsPerLane; ++s)
-    if (ofs[s] != tile0 + lbase + s * kWave + lane) mine_ok = false;
+    if (in.ofs[s] != tile0 + lbase + s * kWave + lane) mine_ok = false;
   if (!mine_ok) lds.irregular = 1;
   __syncthreads();
   const bool onehot = lds.irregular == 0;
@@ -116,7 +133,7 @@ __device__ __forceinline__ void keygen_tile(const KParams& p, const void* __rest
       const uint32_t t = g / p.B;
       const uint32_t b = g - t * p.B;
       const uint32_t r = b * p.T + t;
-      const uint32_t key = item_hash(ix[s], t * p.C, p.TC, p.a, p.b);
+      const uint32_t key = item_hash(in.ix[s], t * p.C, p.TC, p.a, p.b);
       keys[e] = key;
       rows[e] = r;
       if (p.mean && first) inv_len[r] = il;

@@ -172,7 +172,7 @@ __global__ __launch_bounds__(kBlockThreads) void sort_hist_kernel(
 }
 
 // Keygen in item space for batches with as many items as bags, fused with
-// the first radix pass's histogram: one sort tile per workgroup (keygen_tile).
+// the first radix pass's histogram: one sort tile per workgroup.
 template <bool I32>
 __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
     const KParams p, const void* __restrict__ indices, const void* __restrict__ offsets,
@@ -181,7 +181,9 @@ __global__ __launch_bounds__(kBlockThreads) void keygen_hist_kernel(
   const uint32_t tile = sort_tile_index(per_xcd);
   if (tile >= nblocks) return;
   __shared__ KeygenLds lds;
-  keygen_tile<I32, true>(p, indices, offsets, keys, rows, inv_len, counts, nblocks, tile, lds);
+  KeygenIn in;
+  keygen_load<I32, true>(p, indices, offsets, tile, in);
+  keygen_process<I32, true>(p, offsets, keys, rows, inv_len, counts, nblocks, tile, in, lds);
 }
 
 // Scans of the count rows.  A chunk of kScanChunk consecutive entries is

@@ -129,7 +129,12 @@ class ReduceTimer:
     def elapsed_ms(self, i):
         ms = self._ct.c_float()
         st = self.hip.hipEventElapsedTime(self._ct.byref(ms), self.pairs[i][0], self.pairs[i][1])
-        return ms.value if st == 0 else None
+        if st != 0:
+            # events never recorded: clear the runtime's last error, which
+            # the next HIP call (torch's included) would report otherwise
+            self.hip.hipGetLastError()
+            return None
+        return ms.value
 
     def close(self):
         for pair in self.pairs:

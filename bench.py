@@ -33,8 +33,10 @@ Prints one JSON line on stdout; diagnostics go to stderr.
                  reads measured at start-up for the caches (no published
                  figure), reported with the random 64-byte gather rates.
                  Events bracket the calls of every --event-every-th timed step
-                 only: each event record costs the stream about 4 us, which
-                 would otherwise be counted as step time.
+                 only (10 of 100), and the library records events around its
+                 reduce-and-deposit kernel on the steps halfway between (10
+                 more): each event record costs the stream about 4 us, which
+                 is counted as step time.
   cpu_baseline   the CPU oracle timed on a prefix of the same batch
 """
 from __future__ import annotations
@@ -282,7 +284,7 @@ def main():
                     help="no preparation: the backward groups the batch itself")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip measuring the L2 / memory-side cache / HBM denominators")
-    ap.add_argument("--event-every", type=int, default=5,
+    ap.add_argument("--event-every", type=int, default=10,
                     help="time the calls of every n-th timed step with HIP events")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -355,11 +357,11 @@ def main():
     every = max(1, args.event_every)
     evs = {k: [torch.cuda.Event(enable_timing=True) for _ in range(3)]
            for k in range(0, args.steps, every)}
-    # the reduce kernel is timed on steps between the bracketed ones, one in
-    # every 2 * every steps (two more event records per timed call, kept out
-    # of the forward and backward brackets)
+    # the reduce kernel is timed on the steps halfway between the bracketed
+    # ones (two more event records per timed call, kept out of the forward
+    # and backward brackets)
     red_phase = every // 2 if every > 1 else 0
-    red_steps = [k for k in range(args.steps) if k % (2 * every) == red_phase]
+    red_steps = [k for k in range(args.steps) if k % every == red_phase]
     timer = ReduceTimer(len(red_steps))
     red = {k: timer.pairs[i] for i, k in enumerate(red_steps)}
     torch.cuda.synchronize()

@@ -33,10 +33,11 @@ Prints one JSON line on stdout; diagnostics go to stderr.
                  reads measured at start-up for the caches (no published
                  figure), reported with the random 64-byte gather rates.
                  Events bracket the calls of every --event-every-th timed step
-                 only (10 of 100), and the library records events around its
-                 reduce-and-deposit kernel on the steps halfway between (10
-                 more): each event record costs the stream about 4 us, which
-                 is counted as step time.
+                 only (10 of 100): each event record costs the stream about
+                 4 us, which is counted as step time.  On the steps halfway
+                 between (10 more) the library has the dispatch of its
+                 reduce-and-deposit kernel record events at the kernel's start
+                 and end (no commands added to the stream).
   cpu_baseline   the CPU oracle timed on a prefix of the same batch
 """
 from __future__ import annotations
@@ -109,8 +110,9 @@ def counted_traffic(workload: str, kernel: str = "forward_kernel"):
 
 
 class ReduceTimer:
-    """HIP events that the library records around its reduce-and-deposit
-    kernel (pss_debug_reduce_events), one pair per timed call.  A pair the
+    """HIP events recorded at the start and end of the library's
+    reduce-and-deposit kernel (pss_debug_reduce_events), one pair per timed
+    call.  A pair the
     library never recorded (no such kernel on this workload's path) reads
     as None."""
 
@@ -400,8 +402,8 @@ def main():
     step_bound = max(timed, key=lambda lv: timed[lv]["t_star_us"])
     t_star = timed[step_bound]["t_star_us"] * 1e-6
     # Kernels timed live: pss_forward launches exactly one kernel (events
-    # around the call time it); the library records events around its
-    # reduce-and-deposit kernel on request.  Each kernel's bound is the level
+    # around the call time it); the library has the reduce-and-deposit
+    # kernel's dispatch record events at its start and end on request.  Each kernel's bound is the level
     # whose floor time is largest for its own bytes; the roofline object
     # describes the longer of the two (the dominant kernel), and both are
     # listed under "kernels".  Kernel names are those the committed counters

@@ -327,14 +327,15 @@ int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash
                     hipStream_t stream);
 
 /* Timing hook for measurement tools (no part of the method).  With two
- * non-null events (hipEvent_t, created by the caller and kept alive while
- * the hook is set), every later backward call that runs the sorted path's
- * reduce-and-deposit kernel records `before` on the call's stream right
- * before that kernel and `after` right after it, so that the kernel's own
- * duration can be read with hipEventElapsedTime.  Two nulls switch it off;
- * one null and one event is PSS_ERR_INVALID_ARG.  One setting for the whole
- * process: meant for one caller timing its own calls, not for concurrent
- * callers.  Each record adds a few microseconds to the stream. */
+ * non-null events (hipEvent_t, created by the caller with timing enabled and
+ * kept alive while the hook is set), every later backward call that runs
+ * the sorted path's reduce-and-deposit kernel launches it so that its
+ * dispatch records `before` when the kernel starts and `after` when it ends:
+ * hipEventElapsedTime then gives the kernel's own duration, without the
+ * wait for earlier work on the stream or the dispatch.  Two nulls switch it
+ * off; one null and one event is PSS_ERR_INVALID_ARG.  One setting for the
+ * whole process: meant for one caller timing its own calls, not for
+ * concurrent callers. */
 int pss_debug_reduce_events(void* before, void* after);
 
 /* Host evaluation of the same hash code the kernels run (no GPU needed):

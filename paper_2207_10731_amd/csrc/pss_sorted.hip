@@ -23,6 +23,8 @@
 //             add the run's sum at the run's hashed addresses with float
 //             atomics.  A token spanning several pieces deposits one partial
 //             sum per piece.
+#include <hip/hip_ext.h>
+
 #include <atomic>
 
 #include "pss_keygen.hpp"
@@ -849,8 +851,8 @@ hipError_t launch_keygen(const KParams& p, const void* indices, const void* offs
   return hipGetLastError();
 }
 
-// Timing hook (pss_debug_reduce_events): events recorded around each
-// reduce-and-deposit launch, both or neither set.
+// Timing hook (pss_debug_reduce_events): events recorded at the start and
+// end of each reduce-and-deposit kernel, both or neither set.
 static std::atomic<hipEvent_t> g_reduce_before{nullptr}, g_reduce_after{nullptr};
 
 void set_reduce_events(hipEvent_t before, hipEvent_t after) {
@@ -864,17 +866,19 @@ static hipError_t launch_reduce_t(float* dst, float scale, const KParams& p, con
                                   uint32_t* rkey, uint32_t* rval, hipStream_t stream) {
   const uint64_t blocks = (static_cast<uint64_t>(p.N) + kPiece - 1) / kPiece;
   const uint32_t slabs = (p.d + kWave * EPL - 1) / (kWave * EPL);
+  const dim3 grid(static_cast<uint32_t>(blocks), slabs);
   const hipEvent_t before = g_reduce_before.load(), after = g_reduce_after.load();
   if (before != nullptr && after != nullptr) {
-    const hipError_t e = hipEventRecord(before, stream);
-    if (e != hipSuccess) return e;
+    // the kernel's dispatch records both events: they bracket its execution
+    // alone, not the wait for the previous kernel or the dispatch itself
+    hipExtLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT, REC>), grid,
+                          dim3(kReduceThreads), 0, stream, before, after, 0u, dst, scale, p, keys,
+                          rows, grad, inv_len, p.N, rkey, rval);
+  } else {
+    hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT, REC>), grid, dim3(kReduceThreads),
+                       0, stream, dst, scale, p, keys, rows, grad, inv_len, p.N, rkey, rval);
   }
-  hipLaunchKernelGGL((reduce_deposit_kernel<EPL, U, SIGN, GT, REC>),
-                     dim3(static_cast<uint32_t>(blocks), slabs), dim3(kReduceThreads), 0, stream,
-                     dst, scale, p, keys, rows, grad, inv_len, p.N, rkey, rval);
-  hipError_t e = hipGetLastError();
-  if (e == hipSuccess && before != nullptr && after != nullptr) e = hipEventRecord(after, stream);
-  return e;
+  return hipGetLastError();
 }
 
 template <bool SIGN, typename GT, bool REC>

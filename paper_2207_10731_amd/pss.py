@@ -380,11 +380,11 @@ def pss_validate_offsets_host(offsets, num_bags, N) -> int:
 
 
 def pss_debug_reduce_events(before=None, after=None):
-    """Timing hook: later backward calls record the two events (torch.cuda.Event
-    objects recorded once already, so that their HIP events exist, or raw
-    hipEvent_t handles) right before and after their reduce-and-deposit
-    kernel; no arguments switch it off.  The events must stay alive while the
-    hook is set."""
+    """Timing hook: in later backward calls the dispatch of the
+    reduce-and-deposit kernel records the two events (torch.cuda.Event objects
+    with timing, recorded once already so that their HIP events exist, or raw
+    hipEvent_t handles) at the kernel's start and end; no arguments switch it
+    off.  The events must stay alive while the hook is set."""
     handles = []
     for ev in (before, after):
         if ev is None:

@@ -49,9 +49,10 @@ def test_short_tensors_are_refused():
 
 
 def test_reduce_events_hook_brackets_the_reduce_kernel():
-    """With the timing hook set, a sorted backward records both events around
-    its reduce-and-deposit kernel (a positive interval, inside the call's
-    own); the update made with the hook matches the oracle."""
+    """With the timing hook set, the dispatch of a sorted backward's
+    reduce-and-deposit kernel records both events at the kernel's start and
+    end (a positive interval, inside the call's own); the update made with
+    the hook matches the oracle."""
     wl = synth.get("c2").scaled(B=512)
     g = synth.make_grad(wl, B=512)
     L = Layer(wl, flags=pss.PSS_BWD_SORTED)

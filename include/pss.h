@@ -334,8 +334,8 @@ int pss_debug_signs(int64_t M, int32_t Z, int32_t d, const pss_hash_params* hash
  * hipEventElapsedTime then gives the kernel's own duration, without the
  * wait for earlier work on the stream or the dispatch.  Two nulls switch it
  * off; one null and one event is PSS_ERR_INVALID_ARG.  One setting for the
- * whole process: meant for one caller timing its own calls, not for
- * concurrent callers. */
+ * whole process: meant for one caller timing its own calls outside graph
+ * capture, not for concurrent callers. */
 int pss_debug_reduce_events(void* before, void* after);
 
 /* Host evaluation of the same hash code the kernels run (no GPU needed):

@@ -162,6 +162,11 @@ hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, cons
 // arithmetic; bfloat16 storage is widened exactly and rounded once (RNE).
 // ---------------------------------------------------------------------------
 
+// G and the Adagrad state are read (and the state written) non-temporally,
+// the weights through the caches: the memory-side cache then keeps the
+// weights this pass has just written, which the next forward gathers,
+// rather than the state streamed beside them (bfloat16 row-hash workload,
+// 128 MB array and 256 MB state: that forward 881 -> 748 us).
 template <typename WT, bool ADAGRAD>
 __global__ __launch_bounds__(kBlockThreads) void optimizer_kernel(
     WT* __restrict__ w, float* __restrict__ s, const float* __restrict__ G, const int64_t M,
@@ -170,7 +175,9 @@ __global__ __launch_bounds__(kBlockThreads) void optimizer_kernel(
   for (int64_t m = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x; m < M;
        m += stride) {
     const float g = __builtin_nontemporal_load(G + m);
-    if (g != 0.f) apply_update<WT, ADAGRAD>(w, s, m, g, lr, eps);
+    if (g != 0.f)
+      update_loaded<WT, ADAGRAD, true>(w, s, m, g, load_weight64(w, m),
+                                       ADAGRAD ? __builtin_nontemporal_load(s + m) : 0.f, lr, eps);
   }
 }
 

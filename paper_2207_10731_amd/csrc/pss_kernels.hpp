@@ -119,14 +119,18 @@ __device__ __forceinline__ float load_weight64<uint16_t>(const uint16_t* w, int6
 // One element's update from its gradient sum g (g != 0): SGD w -= lr * g, or
 // Adagrad s += g^2, w -= lr * g / (sqrt(s) + eps); float32 arithmetic,
 // bfloat16 storage widened exactly and rounded once.
-// The same with the element's weight (widened) and state already loaded.
-template <typename WT, bool ADAGRAD>
+// The same with the element's weight (widened) and state already loaded;
+// with NT_STATE the new state is stored non-temporally.
+template <typename WT, bool ADAGRAD, bool NT_STATE = false>
 __device__ __forceinline__ void update_loaded(WT* w, float* s, int64_t m, float g, float w_old,
                                               float s_old, float lr, float eps) {
   float upd;
   if (ADAGRAD) {
     const float sn = s_old + g * g;
-    s[m] = sn;
+    if (NT_STATE)
+      __builtin_nontemporal_store(sn, s + m);
+    else
+      s[m] = sn;
     upd = lr * g / (sqrtf(sn) + eps);
   } else {
     upd = lr * g;

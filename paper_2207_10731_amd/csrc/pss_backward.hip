@@ -166,7 +166,7 @@ hipError_t launch_deposit_atomic(float* dst, float scale, const KParams& p, cons
 // the weights through the caches: the memory-side cache then keeps the
 // weights this pass has just written, which the next forward gathers,
 // rather than the state streamed beside them (bfloat16 row-hash workload,
-// 128 MB array and 256 MB state: that forward 881 -> 748 us).
+// 128 MB array and 256 MB state: that forward 876 -> 754 us).
 template <typename WT, bool ADAGRAD>
 __global__ __launch_bounds__(kBlockThreads) void optimizer_kernel(
     WT* __restrict__ w, float* __restrict__ s, const float* __restrict__ G, const int64_t M,
